@@ -1,0 +1,256 @@
+#!/usr/bin/env python3
+"""Packed-KV decode benchmark on one MI355X.
+
+Workload (Llama-3.1-8B-shaped full decode step): 32 layers, 32 query heads,
+8 KV heads (G = 4), d_h = 128, RoPE base 5e5, bf16 inputs, batch 1, 128K
+cached rows, K2V2 (B = 128, b_V = 2), per-(layer, head) widths from the
+greedy allocator on 2048 synthetic calibration tokens.  One step appends and
+quantizes one row for every (layer, KV head) and then runs the split-context
+decode attention of every layer over the packed cache (one all-layer launch
+of each entry point).  Inputs are resident in HBM before timing starts.
+
+Prints one JSON line.  See the design notes for the roofline definitions.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+SEED = 3
+N_LAYERS, N_KV, GROUP, BASE = 32, 8, 4, 5e5
+K_BUDGET, V_BITS = 128, 2
+N_CAL = 2048
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--ctx", type=int, default=131072)
+    ap.add_argument("--n-splits", type=int, default=0)
+    ap.add_argument("--no-fp16", action="store_true", help="skip the fp16 comparator")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+def setup_allocation(bg, synth):
+    """Energy scores and widths from the library (host entry points)."""
+    bits = np.zeros((N_LAYERS, N_KV, 64), np.uint8)
+    sig = np.zeros((N_LAYERS, N_KV, 64))
+    for layer in range(N_LAYERS):
+        for h in range(N_KV):
+            sig[layer, h] = synth.sigma_profile(SEED, layer, h)
+            qc, kc = synth.calibration(SEED, layer, h, N_CAL, GROUP, sig[layer, h])
+            s = bg.blockgtq_energy_scores(qc.astype(np.float32), kc.astype(np.float32))
+            bits[layer, h] = bg.blockgtq_allocate(s, K_BUDGET)[0]
+    return bits, sig
+
+
+def n_groups(bits):
+    return np.array([[len(np.unique(bits[layer, h])) for h in range(bits.shape[1])] for layer in range(bits.shape[0])])
+
+
+def percentile(xs, p):
+    return float(np.percentile(np.asarray(xs), p))
+
+
+def cpu_oracle_baseline(bits, sig, rot_k, rot_v, T, budget_s):
+    """Time the CPU oracle (fp64, rotated form) on a bounded sample: whole
+    (layer, KV head) units of one decode step at full context, each = encode
+    the appended row + attend T+1 rows for the G query heads."""
+    from oracle import blockgtq_oracle as o
+    from paper_2606_24033_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+    units, bytes_done, elapsed = 0, 0.0, 0.0
+    layer = 0
+    while elapsed < budget_s and units < N_LAYERS * N_KV:
+        k, v = synth.torch_layer_kv(SEED, layer, T + 1, sig[layer], BASE)
+        k = k.float().cpu().numpy()
+        v = v.float().cpu().numpy()
+        q = synth.torch_queries(SEED, layer, N_KV * GROUP, [T], BASE)[0].float().cpu().numpy()
+        for h in range(N_KV):
+            kc, widths, kn, _ = o.quantize_keys(k[:T, h], bits[layer, h], rot_k)   # cache contents (untimed)
+            vc, vn, _ = o.quantize_values(v[:T, h], rot_v, V_BITS)
+            t0 = time.perf_counter()
+            kc1, _, kn1, _ = o.quantize_keys(k[T:, h], bits[layer, h], rot_k)
+            vc1, vn1, _ = o.quantize_values(v[T:, h], rot_v, V_BITS)
+            o.attention_rotated(q[h * GROUP:(h + 1) * GROUP], np.concatenate([kc, kc1]), np.concatenate([kn, kn1]),
+                                bits[layer, h], rot_k, np.concatenate([vc, vc1]), np.concatenate([vn, vn1]), rot_v,
+                                V_BITS)
+            elapsed += time.perf_counter() - t0
+            ng = len(np.unique(bits[layer, h]))
+            bytes_done += (T + 1) * (K_BUDGET * 2 / 8 + 2 * ng + 128 * V_BITS / 8 + 2)
+            units += 1
+            if elapsed >= budget_s:
+                break
+        layer += 1
+    return {"value": bytes_done / elapsed / 1e9, "unit": "GB/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{units} of {N_LAYERS * N_KV} (layer, KV head) units of one decode step at ctx {T + 1} "
+                      f"(encode appended row + rotated-form fp64 attention), {elapsed:.1f} s",
+            "us_per_step_equiv": elapsed / units * N_LAYERS * N_KV * 1e6}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); multi-GPU runs are not part of this build.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_24033_amd import blockgtq as bg
+    from paper_2606_24033_amd import synth
+
+    if not torch.cuda.is_available():
+        print("no GPU available", file=sys.stderr)
+        sys.exit(1)
+    bg.lib()
+    T = args.ctx
+    n_extra = args.warmup + args.steps
+    cap = ((T + n_extra + 31) // 32) * 32
+    max_ctx = T + n_extra
+    cfg = bg.Config(n_layers=N_LAYERS, batch=1, n_kv_heads=N_KV, group=GROUP, capacity=cap, k_budget=K_BUDGET,
+                    v_bits=V_BITS, in_dtype=bg.BGTQ_BF16)
+    t_setup = time.time()
+    bits, sig = setup_allocation(bg, synth)
+    rot_k, rot_v = synth.rotations(SEED)
+    layout = bg.Layout(cfg, bits, synth.flat_rot_k(rot_k), rot_v)
+    cache = bg.Cache(cfg)
+    want_fp16 = not args.no_fp16
+    if want_fp16:
+        k16 = torch.zeros((N_LAYERS, 1, N_KV, cap, 128), dtype=torch.float16, device="cuda")
+        v16 = torch.zeros_like(k16)
+    wp0 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for layer in range(N_LAYERS):
+        k, v = synth.torch_layer_kv(SEED, layer, T + n_extra, sig[layer], BASE)
+        bg.blockgtq_quantize_append(cfg, layout, layer, k[None, :T].contiguous(), v[None, :T].contiguous(), wp0,
+                                    cache)
+        if want_fp16:
+            k16[layer, 0, :, :T + n_extra] = k.transpose(0, 1).half()
+            v16[layer, 0, :, :T + n_extra] = v.transpose(0, 1).half()
+        if layer == 0:
+            knew_all = torch.empty((n_extra, N_LAYERS, 1, 1, N_KV, 128), dtype=torch.bfloat16, device="cuda")
+            vnew_all = torch.empty_like(knew_all)
+        knew_all[:, layer, 0, 0] = k[T:]
+        vnew_all[:, layer, 0, 0] = v[T:]
+        del k, v
+    positions = list(range(T, T + n_extra))
+    q_all = torch.stack([synth.torch_queries(SEED, layer, N_KV * GROUP, positions, BASE)
+                         for layer in range(N_LAYERS)], dim=1)[:, :, None].contiguous()   # [steps, L, 1, Hq, 128]
+    wps = torch.arange(T, T + n_extra, dtype=torch.int32, device="cuda")
+    ctxs = wps + 1
+    out = torch.empty((N_LAYERS, 1, N_KV * GROUP, 128), dtype=torch.float32, device="cuda")
+    ws = torch.empty(bg.workspace_bytes(cfg, N_LAYERS, args.n_splits, max_ctx), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    log(f"setup {time.time() - t_setup:.1f} s (prefill of {T} rows x {N_LAYERS} layers x {N_KV} heads)")
+
+    def step(s):
+        bg.blockgtq_quantize_append(cfg, layout, -1, knew_all[s], vnew_all[s], wps[s:s + 1], cache)
+        bg.blockgtq_decode_attn(cfg, layout, -1, q_all[s], ctxs[s:s + 1], max_ctx, cache, out=out, workspace=ws,
+                                n_splits=args.n_splits)
+
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    evd = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    g0.record()
+    for i in range(args.steps):
+        s = args.warmup + i
+        ev[i][0].record()
+        bg.blockgtq_quantize_append(cfg, layout, -1, knew_all[s], vnew_all[s], wps[s:s + 1], cache)
+        evd[i][0].record()
+        bg.blockgtq_decode_attn(cfg, layout, -1, q_all[s], ctxs[s:s + 1], max_ctx, cache, out=out, workspace=ws,
+                                n_splits=args.n_splits)
+        evd[i][1].record()
+        ev[i][1].record()
+    g1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    total_ms = g0.elapsed_time(g1)
+    step_us = [a.elapsed_time(b) * 1e3 for a, b in ev]
+    dec_us = [a.elapsed_time(b) * 1e3 for a, b in evd]
+    ms_per_step = total_ms / args.steps
+    log(f"timed {args.steps} steps: {total_ms:.2f} ms on events, {wall * 1e3:.2f} ms wall")
+
+    ng = n_groups(bits)
+    ctx_mean = T + args.warmup + (args.steps + 1) / 2.0
+    row_bytes = K_BUDGET * 2 / 8 + 128 * V_BITS / 8 + 2     # codes + V norm
+    norm_bytes = 2.0 * ng.sum()                             # K group norms over all (layer, head)
+    step_bytes = ctx_mean * (row_bytes * N_LAYERS * N_KV + norm_bytes)
+    io_bytes = N_LAYERS * N_KV * GROUP * 128 * (2 + 4)      # q in, out
+    step_bytes += io_bytes
+    gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+    dec_med = float(np.median(dec_us))
+    dec_gbs = step_bytes / (dec_med * 1e-6) / 1e9
+
+    result = {
+        "metric": "packed-KV decode attention us/step + effective HBM GB/s (% of peak) at 128K ctx",
+        "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "Llama-3.1-8B-shaped full decode step: 32 layers x 8 KV heads (32 q heads), "
+                               f"d_h 128, {T} cached rows, K2V2, batch 1, bf16 inputs",
+                   "global_batch": 1, "seq_len": T, "parallelism": "none (1 GPU)", "n_splits": args.n_splits},
+        "us_per_step": round(ms_per_step * 1e3, 2),
+        "us_per_step_median": round(float(np.median(step_us)), 2),
+        "us_per_step_p5": round(percentile(step_us, 5), 2), "us_per_step_p95": round(percentile(step_us, 95), 2),
+        "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        "decode_call_us_median": round(dec_med, 2),
+        "packed_bytes_per_step": int(step_bytes),
+        "fp16_bytes_per_step": int(ctx_mean * N_LAYERS * N_KV * 512),
+    }
+    result["roofline"] = {"bound": "hbm", "achieved": round(dec_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                          "kernel": "decode call (q rotation + split pass + merge), all layers, one launch each"}
+
+    if want_fp16:
+        fe = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        out16 = torch.empty_like(out)
+        q16 = [q_all[args.warmup + i] for i in range(args.steps)]
+        for i in range(min(args.warmup, 3)):
+            bg.blockgtq_decode_attn_fp16(cfg, -1, q16[i], ctxs[args.warmup + i:args.warmup + i + 1], max_ctx, k16, v16,
+                                         out=out16, workspace=ws, n_splits=args.n_splits)
+        for i in range(args.steps):
+            s = args.warmup + i
+            fe[i][0].record()
+            bg.blockgtq_decode_attn_fp16(cfg, -1, q16[i], ctxs[s:s + 1], max_ctx, k16, v16, out=out16, workspace=ws,
+                                         n_splits=args.n_splits)
+            fe[i][1].record()
+        torch.cuda.synchronize()
+        f_us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in fe]))
+        fbytes = ctx_mean * N_LAYERS * N_KV * 512
+        result["fp16_decode_us_median"] = round(f_us, 2)
+        result["fp16_decode_gbs"] = round(fbytes / (f_us * 1e-6) / 1e9, 2)
+        result["speedup_vs_fp16_decode"] = round(f_us / dec_med, 3)
+        del k16, v16
+
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_oracle_baseline(bits, sig, rot_k, rot_v, T, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,194 @@
+/*
+ * blockgtq.h -- C ABI of the Block-GTQ packed-cache serving path on MI355X.
+ *
+ * Paper: "RoPE-Aware Bit Allocation for KV-Cache Quantization" (Block-GTQ).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Return value: 0 (BGTQ_OK) on success, a negative BGTQ_E* code on error.
+ *    blockgtq_last_error() returns a message for the calling thread's last
+ *    error.  No C++ exception crosses this boundary.  Argument errors are
+ *    detected on the host before anything is enqueued.
+ *  - Ownership: the caller owns every buffer.  The library never allocates
+ *    device memory and keeps no state between calls; the device layout blob
+ *    built by blockgtq_layout_init holds all constants.
+ *  - Pointers named d_* and the cache / input / output pointers of the async
+ *    calls are device pointers.  Host pointers are named h_* or documented so.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    The async calls only enqueue work; their device inputs must stay alive
+ *    until the stream reaches them.  They neither allocate nor synchronise.
+ *  - Shapes: head_dim d_h = 128 (L = 64 RoPE blocks); RoPE block i is the pair
+ *    of dims (i, i + 64).  Group size G = query heads per KV head.
+ *
+ * Packed cache layout (per layer, sequence and KV head; all little-endian)
+ * ---------------------------------------------------------------------
+ *  k_codes : uint32 [n_layers][batch][n_kv_heads][capacity][k_words]
+ *            One key row = the codes of every same-rate group, groups in
+ *            ascending bit width, inside a group the rotated coordinates in
+ *            order; each code is a dense b-bit field, LSB first; stream bit o
+ *            is bit (o % 32) of word (o / 32).  k_words = ceil(2 B / 32).
+ *  k_norms : fp16  [n_layers][batch][n_kv_heads][8][capacity]
+ *            The radius of each same-rate group (group ordinal, ascending b).
+ *  v_codes : uint32 [n_layers][batch][n_kv_heads][capacity/32][d_h][b_v]
+ *            Tiles of 32 tokens.  For rotated coordinate j the 32 codes of a
+ *            tile form one 32*b_v-bit string; token slot s = t % 32 occupies
+ *            bits [s*b_v, s*b_v + b_v).
+ *  v_norms : fp16  [n_layers][batch][n_kv_heads][capacity]
+ *  capacity must be a multiple of 32.  The caller zero-fills the cache once.
+ */
+#ifndef BLOCKGTQ_H
+#define BLOCKGTQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  BGTQ_OK = 0,
+  BGTQ_EINVAL = -1,       /* bad argument (shape, pointer, value)             */
+  BGTQ_EBUDGET = -2,      /* bit budget outside [L*b_min, L*b_max]            */
+  BGTQ_ECAPACITY = -3,    /* append or context beyond the cache capacity      */
+  BGTQ_EWORKSPACE = -4,   /* workspace smaller than blockgtq_workspace_bytes  */
+  BGTQ_EUNSUPPORTED = -5, /* configuration this build does not handle         */
+  BGTQ_EHIP = -6          /* a HIP runtime call failed (message has details)  */
+};
+
+enum { BGTQ_FP32 = 0, BGTQ_BF16 = 1 };
+
+/* Message for the calling thread's most recent error ("" if none). */
+const char* blockgtq_last_error(void);
+
+typedef struct {
+  int32_t n_layers;    /* layers held by the cache                          */
+  int32_t batch;       /* sequences                                         */
+  int32_t n_kv_heads;  /* KV heads per layer                                */
+  int32_t group;       /* query heads per KV head (G), 1..8                 */
+  int32_t head_dim;    /* d_h; must be 128                                  */
+  int32_t capacity;    /* rows per (layer, sequence, KV head); multiple of 32 */
+  int32_t k_budget;    /* B = sum of the 64 block widths of a key head; the
+                          K row holds 2B bits (K3 -> 192, K2 -> 128)         */
+  int32_t v_bits;      /* b_V, 1..8                                         */
+  int32_t in_dtype;    /* BGTQ_FP32 or BGTQ_BF16 for K, V and Q inputs       */
+} bgtq_config;
+
+typedef struct {
+  void* k_codes; /* device, see layout above */
+  void* k_norms;
+  void* v_codes;
+  void* v_norms;
+} bgtq_cache;
+
+/* ---- (a0) energy score -------------------------------------------------
+ * Eq. (scoring-layer-head-energy) in Sec. 3.1, in its GQA form from the
+ * calibration appendix: for each RoPE block i,
+ *   s_i = 1/2 ( mean over tokens t and heads g of ||q_{g,t}^(i)||^2
+ *               + mean over tokens t of ||k_t^(i)||^2 ).
+ * Host, synchronous.  h_q: float [n_tokens][group][head_dim], h_k: float
+ * [n_tokens][head_dim] (pre- or post-RoPE: block norms are RoPE-invariant).
+ * h_scores_out: double [head_dim/2].  EINVAL on null pointers, n_tokens < 1,
+ * group < 1 or odd head_dim. */
+int blockgtq_energy_scores(const float* h_q, const float* h_k, int32_t n_tokens,
+                           int32_t group, int32_t head_dim, double* h_scores_out);
+
+/* ---- (a1) greedy allocator ---------------------------------------------
+ * Algorithm 1 (Sec. 3.2): minimise J(b) = sum_i s_i 4^-b_i subject to
+ * b_min <= b_i <= b_max and sum_i b_i = budget, by handing out bits one at a
+ * time to the block with the largest marginal gain (3/4) s_i 4^-b_i.
+ * Equal gains go to the lowest block index.  Host, synchronous, pure.
+ * h_scores: double [n_rows][n_blocks], each finite and >= 0 (else EINVAL).
+ * budget in [n_blocks*b_min, n_blocks*b_max] (else EBUDGET);
+ * 1 <= b_min <= b_max <= 8.  h_bits_out: uint8 [n_rows][n_blocks]. */
+int blockgtq_allocate(const double* h_scores, int32_t n_rows, int32_t n_blocks,
+                      int32_t budget, int32_t b_min, int32_t b_max, uint8_t* h_bits_out);
+
+/* ---- codebook ----------------------------------------------------------
+ * The scalar quantizer of TQ-MSE (Sec. 2.2) at b bits: Gaussian Lloyd-Max
+ * centroids rounded to fp16, and the 2^b - 1 decision thresholds (midpoints
+ * of adjacent fp16 centroids, exact in fp32).  Host, synchronous.
+ * h_c16_out: uint16 fp16 bit patterns [2^b]; h_thr_out: float [2^b - 1]
+ * (either may be NULL).  EINVAL unless 1 <= b <= 8. */
+int blockgtq_codebook(int32_t b, uint16_t* h_c16_out, float* h_thr_out);
+
+/* ---- sizing ------------------------------------------------------------ */
+int blockgtq_layout_bytes(const bgtq_config* cfg, size_t* bytes_out);
+int blockgtq_cache_bytes(const bgtq_config* cfg, size_t* k_codes, size_t* k_norms,
+                         size_t* v_codes, size_t* v_norms);
+/* Workspace of one blockgtq_decode_attn call: n_layers_in_call = 1 for a
+ * single layer, cfg->n_layers for layer = -1.  n_splits as passed to the
+ * call (0 = the heuristic for max_ctx). */
+int blockgtq_workspace_bytes(const bgtq_config* cfg, int32_t n_layers_in_call,
+                             int32_t n_splits, int32_t max_ctx, size_t* bytes_out);
+
+/* ---- (a2) layout build --------------------------------------------------
+ * Same-rate grouping (end of Sec. 3.2) and the static layout metadata that
+ * the packed cache needs (Sec. 4): groups G_b = {i : b_i = b} in ascending
+ * b, each block contributing dims (i, i+64); per-position widths and bit
+ * offsets; the rotations and codebooks.  Uploads everything into the
+ * caller's device buffer d_layout (blockgtq_layout_bytes bytes) and waits
+ * for the copy (synchronous).
+ * h_k_bits: uint8 [n_layers][n_kv_heads][64], each row summing to k_budget.
+ * h_rot_k : float, the K rotations for d = 2, 4, ..., 128 concatenated, each
+ *           d x d row-major (Pi maps a group vector x to Pi x); 357760 floats.
+ * h_rot_v : float [128][128], row-major.
+ * Rotations must be orthogonal (not checked beyond finiteness). */
+int blockgtq_layout_init(const bgtq_config* cfg, const uint8_t* h_k_bits,
+                         const float* h_rot_k, const float* h_rot_v, void* d_layout,
+                         void* stream);
+
+/* ---- (a3-a5) quantize + pack + append -----------------------------------
+ * TQ-MSE (Sec. 2.2) per same-rate K group and per V row: n = ||x||,
+ * z = sqrt(d) Pi x / n, code_j = #{thresholds <= z_j}, radius stored fp16;
+ * codes packed into the cache layout above.  Async on `stream`.
+ * layer in [0, n_layers) or -1 for all layers.
+ * d_k, d_v: post-RoPE keys / values in cfg->in_dtype,
+ *   [batch][n_new][n_kv_heads][head_dim]  (layer >= 0), or
+ *   [n_layers][batch][n_new][n_kv_heads][head_dim]  (layer == -1).
+ * d_write_pos: int32 [batch]; sequence b's tokens go to rows
+ *   d_write_pos[b] .. d_write_pos[b] + n_new - 1.  The caller guarantees
+ *   d_write_pos[b] + n_new <= capacity (rows past capacity are not written)
+ *   and advances its own lengths.  Calls touching the same rows must not
+ *   overlap in time. */
+int blockgtq_quantize_append(const bgtq_config* cfg, const void* d_layout, int32_t layer,
+                             const void* d_k, const void* d_v, int32_t n_new,
+                             const int32_t* d_write_pos, const bgtq_cache* cache,
+                             void* stream);
+
+/* ---- (a6-a8) split-context decode attention over the packed cache -------
+ * Sec. 4: each query attends rows [0, d_ctx_len[b]) of its KV head with
+ * logits q . k_hat / sqrt(d_h) and a softmax, the keys and values decoded
+ * from the packed codes inside the kernel (no fp16 cache is written); the
+ * context is split along the key axis into n_splits ranges whose partial
+ * (max, sum, accumulator) states are merged exactly by log-sum-exp.  The
+ * query is rotated into each group's code domain first (the Q-side rotation).
+ * d_q: post-RoPE queries in cfg->in_dtype, [batch][n_kv_heads*group][head_dim]
+ *      (layer >= 0) or [n_layers][batch][...][head_dim] (layer == -1).
+ * d_ctx_len: int32 [batch], each in [0, max_ctx]; a sequence with 0 rows
+ *      gets an all-zero output.
+ * max_ctx: host-side upper bound of d_ctx_len (<= capacity), sizes the splits.
+ * d_out: float, same shape as d_q.
+ * d_workspace / ws_bytes: see blockgtq_workspace_bytes (EWORKSPACE if short).
+ * n_splits: 0 = heuristic, else 1 .. 4096. */
+int blockgtq_decode_attn(const bgtq_config* cfg, const void* d_layout, int32_t layer,
+                         const void* d_q, const int32_t* d_ctx_len, int32_t max_ctx,
+                         const bgtq_cache* cache, float* d_out, void* d_workspace,
+                         size_t ws_bytes, int32_t n_splits, void* stream);
+
+/* ---- fp16 comparator ----------------------------------------------------
+ * The same split-context decode over an uncompressed fp16 cache, the
+ * baseline the packed path's speedup is reported against (the paper compares
+ * with fp16 FlashAttention-2 decode, Sec. 6 deployment).
+ * d_k16, d_v16: fp16 [n_layers][batch][n_kv_heads][capacity][head_dim].
+ * Other arguments as blockgtq_decode_attn (no layout blob: no codes). */
+int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void* d_q,
+                              const int32_t* d_ctx_len, int32_t max_ctx,
+                              const void* d_k16, const void* d_v16, float* d_out,
+                              void* d_workspace, size_t ws_bytes, int32_t n_splits,
+                              void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BLOCKGTQ_H */

@@ -345,33 +345,43 @@ def unpack_key_rows(words: np.ndarray, widths) -> np.ndarray:
 def pack_value_tiles(codes: np.ndarray, b_v: int, t0: int = 0, capacity: int | None = None,
                      into: np.ndarray | None = None) -> np.ndarray:
     """Write value codes of tokens t0 .. t0+n-1 into the tile layout
-    [capacity/32, d_h, b_v] uint32 (zero-initialised unless `into` is given)."""
+    [capacity/32, d_h, b_v] uint32 (zero-initialised unless `into` is given;
+    the bits of other tokens in `into` are kept)."""
     n, d = codes.shape
     if capacity is None:
         capacity = ((t0 + n + 31) // 32) * 32
     out = np.zeros((capacity // 32, d, b_v), dtype=np.uint64) if into is None else into.astype(np.uint64)
-    for t in range(n):
-        tok = t0 + t
-        tile, s = divmod(tok, 32)
+    tok = np.arange(t0, t0 + n)
+    for s in range(32):                      # token slot inside a tile
+        sel = tok % 32 == s
+        if not np.any(sel):
+            continue
+        tiles = tok[sel] // 32
         o = s * b_v
-        val = codes[t].astype(np.uint64) << np.uint64(o % 32)
-        out[tile, :, o // 32] |= val & np.uint64(0xFFFFFFFF)
+        val = codes[sel].astype(np.uint64) << np.uint64(o % 32)
+        field = np.uint64((1 << b_v) - 1) << np.uint64(o % 32)
+        out[tiles, :, o // 32] &= ~(field & np.uint64(0xFFFFFFFF))
+        out[tiles, :, o // 32] |= val & np.uint64(0xFFFFFFFF)
         if o % 32 + b_v > 32:
-            out[tile, :, o // 32 + 1] |= val >> np.uint64(32)
+            out[tiles, :, o // 32 + 1] &= ~(field >> np.uint64(32))
+            out[tiles, :, o // 32 + 1] |= val >> np.uint64(32)
     return out.astype(np.uint32)
 
 
 def unpack_value_tiles(tiles: np.ndarray, b_v: int, n: int, t0: int = 0) -> np.ndarray:
     w64 = tiles.astype(np.uint64)
-    d = tiles.shape[1]
-    out = np.zeros((n, d), dtype=np.int64)
-    for t in range(n):
-        tile, s = divmod(t0 + t, 32)
+    out = np.zeros((n, tiles.shape[1]), dtype=np.int64)
+    tok = np.arange(t0, t0 + n)
+    for s in range(32):
+        sel = tok % 32 == s
+        if not np.any(sel):
+            continue
+        tl = tok[sel] // 32
         o = s * b_v
-        v = w64[tile, :, o // 32] >> np.uint64(o % 32)
+        v = w64[tl, :, o // 32] >> np.uint64(o % 32)
         if o % 32 + b_v > 32:
-            v |= w64[tile, :, o // 32 + 1] << np.uint64(32 - o % 32)
-        out[t] = (v & np.uint64((1 << b_v) - 1)).astype(np.int64)
+            v |= w64[tl, :, o // 32 + 1] << np.uint64(32 - o % 32)
+        out[sel] = (v & np.uint64((1 << b_v) - 1)).astype(np.int64)
     return out
 
 

@@ -1,0 +1,504 @@
+// Host side of the C ABI declared in include/blockgtq.h: argument checking,
+// the energy score and greedy allocator (host work), the scalar codebook, the
+// layout blob builder, and the launch of the HIP kernels.
+#include "blockgtq.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <queue>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "layout.h"
+
+using namespace bgtq;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return BGTQ_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(BGTQ_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---------------------------------------------------------------- fp16 bits
+// Round a double to the nearest fp16 (ties to even); finite inputs only.
+uint16_t f64_to_f16_bits(double x) {
+  uint16_t sign = std::signbit(x) ? 0x8000 : 0;
+  double a = std::fabs(x);
+  if (a == 0.0) return sign;
+  int e;
+  std::frexp(a, &e);          // a = m 2^e, m in [0.5, 1)
+  int E = e - 1;              // a = 1.f 2^E
+  if (E < -14) E = -14;       // subnormal range shares the 2^-24 quantum
+  double quantum = std::ldexp(1.0, E - 10);
+  double q = std::nearbyint(a / quantum);  // default rounding: to nearest, ties even
+  if (q >= 2048.0) {          // mantissa overflowed into the next binade
+    q /= 2.0;
+    E += 1;
+  }
+  if (E > 15) return sign | 0x7C00;   // overflow -> inf
+  uint32_t mant = static_cast<uint32_t>(q);
+  if (mant < 1024) return sign | static_cast<uint16_t>(mant);  // subnormal
+  return sign | static_cast<uint16_t>(((E + 15) << 10) | (mant - 1024));
+}
+
+double f16_bits_to_f64(uint16_t h) {
+  int exp = (h >> 10) & 0x1F, mant = h & 0x3FF;
+  double v = exp == 0 ? std::ldexp(static_cast<double>(mant), -24)
+                      : std::ldexp(static_cast<double>(mant + 1024), exp - 25);
+  return (h & 0x8000) ? -v : v;
+}
+
+// --------------------------------------------------- Gaussian Lloyd-Max quantizer
+double npdf(double x) { return std::isfinite(x) ? std::exp(-0.5 * x * x) / std::sqrt(2.0 * M_PI) : 0.0; }
+// upper tail Q(x) = P(X > x)
+double ntail(double x) { return 0.5 * std::erfc(x / std::sqrt(2.0)); }
+
+double prob_between(double lo, double hi) {
+  // P(lo <= X < hi) computed from the tail on the side where it is small
+  if (lo >= 0) return ntail(lo) - ntail(hi);
+  return ntail(-hi) - ntail(-lo);
+}
+
+double inv_normal(double p) {
+  double lo = -40.0, hi = 40.0;
+  for (int it = 0; it < 200; ++it) {
+    double mid = 0.5 * (lo + hi);
+    if (1.0 - ntail(mid) < p) lo = mid; else hi = mid;
+  }
+  return 0.5 * (lo + hi);
+}
+
+// Centroids of the 2^b-level minimum-MSE quantizer of N(0,1): fixed point of
+// c_k = E[X | t_{k-1} <= X < t_k], t_k = (c_k + c_{k+1}) / 2.  Newton steps on
+// F(c) = m(c) - c, whose Jacobian is tridiagonal (Thomas algorithm).
+std::vector<double> lloyd_max(int b) {
+  const int n = 1 << b;
+  std::vector<double> c(n), t(n + 1), m(n), lo_d(n), hi_d(n);
+  for (int k = 0; k < n; ++k) c[k] = std::sqrt(3.0) * inv_normal((k + 0.5) / n);
+  auto eval = [&](const std::vector<double>& cc) {
+    t[0] = -INFINITY;
+    t[n] = INFINITY;
+    for (int k = 1; k < n; ++k) t[k] = 0.5 * (cc[k - 1] + cc[k]);
+    for (int k = 0; k < n; ++k) {
+      double p = prob_between(t[k], t[k + 1]);
+      m[k] = (npdf(t[k]) - npdf(t[k + 1])) / p;
+      lo_d[k] = std::isfinite(t[k]) ? npdf(t[k]) * (m[k] - t[k]) / p : 0.0;        // dm_k/dt_k
+      hi_d[k] = std::isfinite(t[k + 1]) ? npdf(t[k + 1]) * (t[k + 1] - m[k]) / p : 0.0;  // dm_k/dt_{k+1}
+    }
+  };
+  std::vector<double> a(n), dg(n), up(n), rhs(n);
+  for (int it = 0; it < 300; ++it) {
+    eval(c);
+    // (I - J) step = m - c; J[k][k-1] = lo_d/2, J[k][k] = (lo_d+hi_d)/2, J[k][k+1] = hi_d/2
+    for (int k = 0; k < n; ++k) {
+      a[k] = -0.5 * lo_d[k];
+      dg[k] = 1.0 - 0.5 * (lo_d[k] + hi_d[k]);
+      up[k] = -0.5 * hi_d[k];
+      rhs[k] = m[k] - c[k];
+    }
+    for (int k = 1; k < n; ++k) {
+      double w = a[k] / dg[k - 1];
+      dg[k] -= w * up[k - 1];
+      rhs[k] -= w * rhs[k - 1];
+    }
+    std::vector<double> step(n);
+    step[n - 1] = rhs[n - 1] / dg[n - 1];
+    for (int k = n - 2; k >= 0; --k) step[k] = (rhs[k] - up[k] * step[k + 1]) / dg[k];
+    double lam = 1.0, mx = 0.0;
+    std::vector<double> nc(n);
+    for (;;) {  // damp until the centroids stay increasing
+      bool mono = true;
+      for (int k = 0; k < n; ++k) nc[k] = c[k] + lam * step[k];
+      for (int k = 1; k < n; ++k) mono = mono && nc[k] > nc[k - 1];
+      if (mono || lam < 1e-6) break;
+      lam *= 0.5;
+    }
+    for (int k = 0; k < n; ++k) {
+      mx = std::max(mx, std::fabs(nc[k] - c[k]));
+      c[k] = nc[k];
+    }
+    for (int k = 0; k < n / 2; ++k) {  // exact antisymmetry
+      double v = 0.5 * (c[n - 1 - k] - c[k]);
+      c[k] = -v;
+      c[n - 1 - k] = v;
+    }
+    if (mx < 1e-15) break;
+  }
+  return c;
+}
+
+struct Codebooks {
+  uint16_t c16[kCodebookEntries];
+  float thr[kThresholdEntries];
+  Codebooks() {
+    for (int b = 1; b <= 8; ++b) {
+      std::vector<double> c = lloyd_max(b);
+      const int n = 1 << b;
+      for (int k = 0; k < n; ++k) c16[cb_index(b) + k] = f64_to_f16_bits(c[k]);
+      for (int k = 0; k + 1 < n; ++k)
+        thr[thr_index(b) + k] = static_cast<float>(
+            0.5 * (f16_bits_to_f64(c16[cb_index(b) + k]) + f16_bits_to_f64(c16[cb_index(b) + k + 1])));
+    }
+  }
+};
+
+const Codebooks& codebooks() {
+  static const Codebooks cb;  // thread-safe one-time init
+  return cb;
+}
+
+// ------------------------------------------------------------------ configs
+int check_cfg(const bgtq_config* c) {
+  if (!c) return fail(BGTQ_EINVAL, "config is NULL");
+  if (c->head_dim != kHeadDim) return fail(BGTQ_EUNSUPPORTED, "head_dim %d unsupported (only 128)", c->head_dim);
+  if (c->n_layers < 1 || c->batch < 1 || c->n_kv_heads < 1)
+    return fail(BGTQ_EINVAL, "n_layers, batch and n_kv_heads must be >= 1");
+  if (c->group < 1 || c->group > 8) return fail(BGTQ_EUNSUPPORTED, "group %d outside 1..8", c->group);
+  if (c->capacity < kTile || c->capacity % kTile != 0)
+    return fail(BGTQ_EINVAL, "capacity %d must be a positive multiple of 32", c->capacity);
+  if (c->k_budget < kBlocks || c->k_budget > 8 * kBlocks)
+    return fail(BGTQ_EBUDGET, "k_budget %d outside [64, 512]", c->k_budget);
+  if (c->v_bits < 1 || c->v_bits > 8) return fail(BGTQ_EINVAL, "v_bits %d outside 1..8", c->v_bits);
+  if (c->in_dtype != BGTQ_FP32 && c->in_dtype != BGTQ_BF16) return fail(BGTQ_EINVAL, "in_dtype %d", c->in_dtype);
+  return BGTQ_OK;
+}
+
+int k_words_of(const bgtq_config* c) { return (2 * c->k_budget + 31) / 32; }
+
+Dims dims_of(const bgtq_config* c, int layer) {
+  Dims d;
+  d.n_layers = c->n_layers;
+  d.batch = c->batch;
+  d.n_kv = c->n_kv_heads;
+  d.group = c->group;
+  d.capacity = c->capacity;
+  d.k_words = k_words_of(c);
+  d.v_bits = c->v_bits;
+  d.in_dtype = c->in_dtype;
+  d.layer = layer;
+  d.n_lc = layer < 0 ? c->n_layers : 1;
+  return d;
+}
+
+struct SplitPlan {
+  int n_splits, split_len;
+};
+
+SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested) {
+  SplitPlan p;
+  if (max_ctx <= 0) return {1, kTile};
+  const int max_splits = (max_ctx + kTile - 1) / kTile;
+  int n;
+  if (requested > 0) {
+    n = std::min(requested, max_splits);
+  } else {
+    const long units = static_cast<long>(c->n_kv_heads) * c->batch * n_lc;
+    n = static_cast<int>((2048 + units - 1) / units);
+    n = std::max(1, std::min(n, (max_ctx + 255) / 256));
+  }
+  p.split_len = ((max_ctx + n - 1) / n + kTile - 1) / kTile * kTile;
+  p.n_splits = (max_ctx + p.split_len - 1) / p.split_len;
+  return p;
+}
+
+size_t al256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+size_t ws_bytes_of(const bgtq_config* c, int n_lc, const SplitPlan& p) {
+  const size_t hq = static_cast<size_t>(c->n_kv_heads) * c->group;
+  const size_t units = static_cast<size_t>(n_lc) * c->batch * hq;
+  return al256(units * kHeadDim * 4) + al256(units * p.n_splits * 130 * 4);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* blockgtq_last_error(void) { return g_err.c_str(); }
+
+int blockgtq_energy_scores(const float* h_q, const float* h_k, int32_t n_tokens, int32_t group,
+                           int32_t head_dim, double* h_scores_out) {
+  if (!h_q || !h_k || !h_scores_out) return fail(BGTQ_EINVAL, "NULL pointer");
+  if (n_tokens < 1 || group < 1 || head_dim < 2 || head_dim % 2)
+    return fail(BGTQ_EINVAL, "bad shape n_tokens=%d group=%d head_dim=%d", n_tokens, group, head_dim);
+  const int L = head_dim / 2;
+  for (int i = 0; i < L; ++i) {
+    double qs = 0.0, ks = 0.0;
+    for (int t = 0; t < n_tokens; ++t) {
+      for (int g = 0; g < group; ++g) {
+        const float* q = h_q + (static_cast<size_t>(t) * group + g) * head_dim;
+        qs += static_cast<double>(q[i]) * q[i] + static_cast<double>(q[i + L]) * q[i + L];
+      }
+      const float* k = h_k + static_cast<size_t>(t) * head_dim;
+      ks += static_cast<double>(k[i]) * k[i] + static_cast<double>(k[i + L]) * k[i + L];
+    }
+    h_scores_out[i] = 0.5 * (qs / (static_cast<double>(n_tokens) * group) + ks / n_tokens);
+  }
+  return ok();
+}
+
+int blockgtq_allocate(const double* h_scores, int32_t n_rows, int32_t n_blocks, int32_t budget,
+                      int32_t b_min, int32_t b_max, uint8_t* h_bits_out) {
+  if (!h_scores || !h_bits_out) return fail(BGTQ_EINVAL, "NULL pointer");
+  if (n_rows < 0 || n_blocks < 1) return fail(BGTQ_EINVAL, "bad shape");
+  if (b_min < 1 || b_max > 8 || b_min > b_max) return fail(BGTQ_EINVAL, "bounds must satisfy 1 <= b_min <= b_max <= 8");
+  if (budget < n_blocks * b_min || budget > n_blocks * b_max)
+    return fail(BGTQ_EBUDGET, "budget %d outside [%d, %d]", budget, n_blocks * b_min, n_blocks * b_max);
+  for (long i = 0; i < static_cast<long>(n_rows) * n_blocks; ++i)
+    if (!std::isfinite(h_scores[i]) || h_scores[i] < 0.0)
+      return fail(BGTQ_EINVAL, "score %ld is negative or not finite", i);
+  struct Item {
+    double key;
+    int idx;
+  };
+  // largest key first; equal keys -> lowest index first
+  auto worse = [](const Item& a, const Item& b) { return a.key < b.key || (a.key == b.key && a.idx > b.idx); };
+  for (int r = 0; r < n_rows; ++r) {
+    const double* s = h_scores + static_cast<size_t>(r) * n_blocks;
+    uint8_t* bits = h_bits_out + static_cast<size_t>(r) * n_blocks;
+    std::priority_queue<Item, std::vector<Item>, decltype(worse)> pq(worse);
+    for (int i = 0; i < n_blocks; ++i) {
+      bits[i] = static_cast<uint8_t>(b_min);
+      // the marginal gain (3/4) s 4^-b is ordered exactly like s 4^-b
+      if (b_min < b_max) pq.push({std::ldexp(s[i], -2 * b_min), i});
+    }
+    int extra = budget - n_blocks * b_min;
+    while (extra > 0 && !pq.empty()) {
+      Item it = pq.top();
+      pq.pop();
+      int b = ++bits[it.idx];
+      --extra;
+      if (b < b_max) pq.push({std::ldexp(s[it.idx], -2 * b), it.idx});
+    }
+  }
+  return ok();
+}
+
+int blockgtq_codebook(int32_t b, uint16_t* h_c16_out, float* h_thr_out) {
+  if (b < 1 || b > 8) return fail(BGTQ_EINVAL, "b %d outside 1..8", b);
+  const Codebooks& cb = codebooks();
+  if (h_c16_out) std::memcpy(h_c16_out, cb.c16 + cb_index(b), sizeof(uint16_t) << b);
+  if (h_thr_out) std::memcpy(h_thr_out, cb.thr + thr_index(b), sizeof(float) * ((1 << b) - 1));
+  return ok();
+}
+
+int blockgtq_layout_bytes(const bgtq_config* cfg, size_t* bytes_out) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!bytes_out) return fail(BGTQ_EINVAL, "NULL pointer");
+  *bytes_out = layout_total_bytes(cfg->n_layers * cfg->n_kv_heads);
+  return ok();
+}
+
+int blockgtq_cache_bytes(const bgtq_config* cfg, size_t* k_codes, size_t* k_norms, size_t* v_codes,
+                         size_t* v_norms) {
+  if (int e = check_cfg(cfg)) return e;
+  const size_t rows = static_cast<size_t>(cfg->n_layers) * cfg->batch * cfg->n_kv_heads;
+  const size_t cap = cfg->capacity;
+  if (k_codes) *k_codes = rows * cap * k_words_of(cfg) * 4;
+  if (k_norms) *k_norms = rows * kMaxGroups * cap * 2;
+  if (v_codes) *v_codes = rows * cap * kHeadDim * cfg->v_bits / 8;
+  if (v_norms) *v_norms = rows * cap * 2;
+  return ok();
+}
+
+int blockgtq_workspace_bytes(const bgtq_config* cfg, int32_t n_layers_in_call, int32_t n_splits,
+                             int32_t max_ctx, size_t* bytes_out) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!bytes_out) return fail(BGTQ_EINVAL, "NULL pointer");
+  if (n_layers_in_call != 1 && n_layers_in_call != cfg->n_layers)
+    return fail(BGTQ_EINVAL, "n_layers_in_call must be 1 or n_layers");
+  if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);
+  if (max_ctx < 0 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [0, capacity]", max_ctx);
+  *bytes_out = ws_bytes_of(cfg, n_layers_in_call, plan_splits(cfg, n_layers_in_call, max_ctx, n_splits));
+  return ok();
+}
+
+int blockgtq_layout_init(const bgtq_config* cfg, const uint8_t* h_k_bits, const float* h_rot_k,
+                         const float* h_rot_v, void* d_layout, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!h_k_bits || !h_rot_k || !h_rot_v || !d_layout) return fail(BGTQ_EINVAL, "NULL pointer");
+  const int n_rows = cfg->n_layers * cfg->n_kv_heads;
+  const size_t total = layout_total_bytes(n_rows);
+  std::vector<uint8_t> blob(total, 0);
+
+  Header* H = reinterpret_cast<Header*>(blob.data());
+  H->magic = kMagic;
+  H->n_rows = n_rows;
+  H->n_kv_heads = cfg->n_kv_heads;
+  H->k_words = k_words_of(cfg);
+  H->v_bits = cfg->v_bits;
+  H->off_c16 = kOffC16;
+  H->off_thr = kOffThr;
+  H->off_rotv = kOffRotV;
+  H->off_rotvt = kOffRotVT;
+  H->off_rotkt = kOffRotKT;
+  H->off_rows = kOffRows;
+  H->total_bytes = total;
+
+  const Codebooks& cb = codebooks();
+  std::memcpy(blob.data() + kOffC16, cb.c16, sizeof(cb.c16));
+  std::memcpy(blob.data() + kOffThr, cb.thr, sizeof(cb.thr));
+
+  float* rotv = reinterpret_cast<float*>(blob.data() + kOffRotV);
+  float* rotvt = reinterpret_cast<float*>(blob.data() + kOffRotVT);
+  for (int r = 0; r < kHeadDim; ++r)
+    for (int q = 0; q < kHeadDim; ++q) {
+      const float v = h_rot_v[r * kHeadDim + q];
+      if (!std::isfinite(v)) return fail(BGTQ_EINVAL, "rot_v has a non-finite entry");
+      rotv[r * kHeadDim + q] = v;
+      rotvt[q * kHeadDim + r] = v;
+    }
+  float* rotkt = reinterpret_cast<float*>(blob.data() + kOffRotKT);
+  for (int dd = 2; dd <= kHeadDim; dd += 2) {
+    const float* src = h_rot_k + rotk_index(dd);
+    float* dst = rotkt + rotk_index(dd);
+    for (int r = 0; r < dd; ++r)
+      for (int q = 0; q < dd; ++q) {
+        const float v = src[r * dd + q];
+        if (!std::isfinite(v)) return fail(BGTQ_EINVAL, "rot_k (d=%d) has a non-finite entry", dd);
+        dst[q * dd + r] = v;
+      }
+  }
+
+  RowMeta* rows = reinterpret_cast<RowMeta*>(blob.data() + kOffRows);
+  for (int r = 0; r < n_rows; ++r) {
+    const uint8_t* bits = h_k_bits + static_cast<size_t>(r) * kBlocks;
+    int sum = 0;
+    for (int i = 0; i < kBlocks; ++i) {
+      if (bits[i] < 1 || bits[i] > 8) return fail(BGTQ_EINVAL, "row %d block %d: width %d outside 1..8", r, i, bits[i]);
+      sum += bits[i];
+    }
+    if (sum != cfg->k_budget) return fail(BGTQ_EBUDGET, "row %d: widths sum to %d, k_budget is %d", r, sum, cfg->k_budget);
+    RowMeta& M = rows[r];
+    int p = 0, off = 0, g = 0;
+    for (int b = 1; b <= 8; ++b) {
+      int start = p;
+      for (int i = 0; i < kBlocks; ++i) {
+        if (bits[i] != b) continue;
+        for (int dim : {i, i + kBlocks}) {
+          M.dim[p] = static_cast<uint8_t>(dim);
+          M.width[p] = static_cast<uint8_t>(b);
+          M.bitoff[p] = static_cast<uint16_t>(off);
+          M.grp[p] = static_cast<uint8_t>(g);
+          off += b;
+          ++p;
+        }
+      }
+      if (p > start) {
+        M.g_bits[g] = b;
+        M.g_dim[g] = p - start;
+        M.g_pos[g] = start;
+        ++g;
+      }
+    }
+    M.n_groups = g;
+    for (int w = 0; w < kMaxKWords; ++w) {
+      int first = kHeadDim;
+      for (int q = 0; q < kHeadDim; ++q)
+        if (M.bitoff[q] + M.width[q] > 32 * w) {
+          first = q;
+          break;
+        }
+      M.word_first[w] = first;
+    }
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(d_layout, blob.data(), total, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(layout)");
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize(layout)");
+  return ok();
+}
+
+int blockgtq_quantize_append(const bgtq_config* cfg, const void* d_layout, int32_t layer,
+                             const void* d_k, const void* d_v, int32_t n_new,
+                             const int32_t* d_write_pos, const bgtq_cache* cache, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!d_layout || !d_write_pos || !cache || !cache->k_codes || !cache->k_norms || !cache->v_codes ||
+      !cache->v_norms)
+    return fail(BGTQ_EINVAL, "NULL pointer");
+  if (layer < -1 || layer >= cfg->n_layers) return fail(BGTQ_EINVAL, "layer %d out of range", layer);
+  if (n_new < 0) return fail(BGTQ_EINVAL, "n_new %d < 0", n_new);
+  if (n_new > cfg->capacity) return fail(BGTQ_ECAPACITY, "n_new %d > capacity %d", n_new, cfg->capacity);
+  if (n_new == 0) return ok();
+  if (!d_k || !d_v) return fail(BGTQ_EINVAL, "NULL pointer");
+  CachePtrs c{static_cast<uint32_t*>(cache->k_codes), static_cast<uint16_t*>(cache->k_norms),
+              static_cast<uint32_t*>(cache->v_codes), static_cast<uint16_t*>(cache->v_norms)};
+  hipError_t e = launch_quantize_append(dims_of(cfg, layer), d_layout, d_k, d_v, n_new, d_write_pos, c,
+                                        static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "quantize_append launch");
+  return ok();
+}
+
+static int check_decode_args(const bgtq_config* cfg, int32_t layer, const void* d_q, const int32_t* d_ctx_len,
+                             int32_t max_ctx, float* d_out, void* d_ws, size_t ws_bytes, int32_t n_splits,
+                             DecodeWs* ws) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!d_q || !d_ctx_len || !d_out || !d_ws) return fail(BGTQ_EINVAL, "NULL pointer");
+  if (layer < -1 || layer >= cfg->n_layers) return fail(BGTQ_EINVAL, "layer %d out of range", layer);
+  if (max_ctx < 0 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [0, capacity]", max_ctx);
+  if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);
+  const int n_lc = layer < 0 ? cfg->n_layers : 1;
+  const SplitPlan p = plan_splits(cfg, n_lc, max_ctx, n_splits);
+  const size_t need = ws_bytes_of(cfg, n_lc, p);
+  if (ws_bytes < need) return fail(BGTQ_EWORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  const size_t units = static_cast<size_t>(n_lc) * cfg->batch * cfg->n_kv_heads * cfg->group;
+  ws->qp = static_cast<float*>(d_ws);
+  ws->part = reinterpret_cast<float*>(static_cast<uint8_t*>(d_ws) + al256(units * kHeadDim * 4));
+  ws->n_splits = p.n_splits;
+  ws->split_len = p.split_len;
+  return BGTQ_OK;
+}
+
+int blockgtq_decode_attn(const bgtq_config* cfg, const void* d_layout, int32_t layer, const void* d_q,
+                         const int32_t* d_ctx_len, int32_t max_ctx, const bgtq_cache* cache, float* d_out,
+                         void* d_workspace, size_t ws_bytes, int32_t n_splits, void* stream) {
+  DecodeWs ws;
+  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws))
+    return e;
+  if (!d_layout || !cache || !cache->k_codes || !cache->k_norms || !cache->v_codes || !cache->v_norms)
+    return fail(BGTQ_EINVAL, "NULL pointer");
+  CachePtrs c{static_cast<uint32_t*>(cache->k_codes), static_cast<uint16_t*>(cache->k_norms),
+              static_cast<uint32_t*>(cache->v_codes), static_cast<uint16_t*>(cache->v_norms)};
+  hipError_t e = launch_decode_packed(dims_of(cfg, layer), d_layout, d_q, d_ctx_len, c, d_out, ws,
+                                      static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "decode_attn launch");
+  return ok();
+}
+
+int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void* d_q, const int32_t* d_ctx_len,
+                              int32_t max_ctx, const void* d_k16, const void* d_v16, float* d_out,
+                              void* d_workspace, size_t ws_bytes, int32_t n_splits, void* stream) {
+  DecodeWs ws;
+  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws))
+    return e;
+  if (!d_k16 || !d_v16) return fail(BGTQ_EINVAL, "NULL pointer");
+  hipError_t e = launch_decode_fp16(dims_of(cfg, layer), d_q, d_ctx_len, d_k16, d_v16, d_out, ws,
+                                    static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "decode_attn_fp16 launch");
+  return ok();
+}
+
+}  // extern "C"

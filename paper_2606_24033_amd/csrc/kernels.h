@@ -1,0 +1,42 @@
+// Launchers of the HIP kernels (internal; the public surface is blockgtq.h).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace bgtq {
+
+struct Dims {
+  int n_layers, batch, n_kv, group, capacity, k_words, v_bits, in_dtype;
+  int layer;      // >= 0: one layer; -1: all layers
+  int n_lc;       // layers in this call (1 or n_layers)
+};
+
+struct CachePtrs {
+  uint32_t* k_codes;
+  uint16_t* k_norms;
+  uint32_t* v_codes;
+  uint16_t* v_norms;
+};
+
+hipError_t launch_quantize_append(const Dims& d, const void* layout, const void* k,
+                                  const void* v, int n_new, const int32_t* write_pos,
+                                  const CachePtrs& c, hipStream_t s);
+
+// Workspace carve-up of one decode call.
+struct DecodeWs {
+  float* qp;        // [n_lc][batch][Hq][128] rotated, scaled queries
+  float* part;      // [n_lc][batch][Hq][n_splits][130] (m, l, acc[128])
+  int n_splits;     // splits actually launched
+  int split_len;    // tokens per split, multiple of 32
+};
+
+hipError_t launch_decode_packed(const Dims& d, const void* layout, const void* q,
+                                const int32_t* ctx_len, const CachePtrs& c, float* out,
+                                const DecodeWs& ws, hipStream_t s);
+
+hipError_t launch_decode_fp16(const Dims& d, const void* q, const int32_t* ctx_len,
+                              const void* k16, const void* v16, float* out,
+                              const DecodeWs& ws, hipStream_t s);
+
+}  // namespace bgtq

@@ -1,0 +1,75 @@
+// Device-resident layout blob shared by the host setup code and the kernels.
+//
+// The blob holds every constant of the packed cache: the fp16 codebooks and
+// decision thresholds of the scalar quantizer (TQ-MSE, Sec. 2.2), the shared
+// rotations, and per (layer, KV head) the same-rate grouping of the key row
+// (end of Sec. 3.2) flattened into per-position tables.
+#pragma once
+#include <stdint.h>
+
+namespace bgtq {
+
+constexpr int kHeadDim = 128;        // d_h
+constexpr int kBlocks = 64;          // L = d_h / 2 RoPE blocks
+constexpr int kTile = 32;            // tokens per value tile
+constexpr int kMaxGroups = 8;        // same-rate groups (b = 1..8)
+constexpr int kMaxKWords = 32;       // 128 positions x 8 bits / 32
+constexpr int kCodebookEntries = 510;   // sum_b 2^b, b = 1..8
+constexpr int kThresholdEntries = 502;  // sum_b (2^b - 1)
+constexpr int kRotKFloats = 357760;     // sum over d = 2..128 (even) of d*d
+constexpr uint32_t kMagic = 0x51544742u;  // "BGTQ"
+
+__host__ __device__ constexpr int cb_index(int b) { return (1 << b) - 2; }
+__host__ __device__ constexpr int thr_index(int b) { return (1 << b) - 1 - b; }
+// float offset of the d x d K rotation inside the K rotation block
+__host__ __device__ constexpr int rotk_index(int d) {
+  // sum_{e=2,4,..,d-2} e^2 = 4 * sum_{m=1}^{d/2-1} m^2
+  return 4 * ((d / 2 - 1) * (d / 2) * (d - 1) / 6);
+}
+
+// Per (layer, KV head) description of one key row (stream order).
+struct RowMeta {
+  uint8_t dim[kHeadDim];       // stream position -> source dim of the key
+  uint8_t width[kHeadDim];     // code width of the position (bits)
+  uint16_t bitoff[kHeadDim];   // first bit of the position's code in the row
+  uint8_t grp[kHeadDim];       // group ordinal of the position
+  int32_t n_groups;
+  int32_t g_bits[kMaxGroups];  // width of group g
+  int32_t g_dim[kMaxGroups];   // d_g = 2 |G_b|
+  int32_t g_pos[kMaxGroups];   // first stream position of group g
+  int32_t word_first[kMaxKWords];  // first position whose code touches word w
+  int32_t pad[39];
+};
+static_assert(sizeof(RowMeta) == 1024, "RowMeta size");
+
+struct Header {
+  uint32_t magic;
+  int32_t n_rows;        // n_layers * n_kv_heads
+  int32_t n_kv_heads;
+  int32_t k_words;
+  int32_t v_bits;
+  int32_t pad0[3];
+  uint64_t off_c16;      // uint16 [510]   fp16 centroids, b-th table at cb_index(b)
+  uint64_t off_thr;      // float  [502]   thresholds, b-th table at thr_index(b)
+  uint64_t off_rotv;     // float  [128][128] Pi_V row-major
+  uint64_t off_rotvt;    // float  [128][128] Pi_V transposed
+  uint64_t off_rotkt;    // float  [kRotKFloats] each Pi_d transposed, at rotk_index(d)
+  uint64_t off_rows;     // RowMeta [n_rows]
+  uint64_t total_bytes;
+  uint64_t pad1[5];
+};
+static_assert(sizeof(Header) == 128, "Header size");
+
+// Byte offsets of the blob's sections (fixed; only the RowMeta count varies).
+__host__ __device__ constexpr uint64_t align256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+constexpr uint64_t kOffC16 = align256(sizeof(Header));
+constexpr uint64_t kOffThr = align256(kOffC16 + 2 * kCodebookEntries);
+constexpr uint64_t kOffRotV = align256(kOffThr + 4 * kThresholdEntries);
+constexpr uint64_t kOffRotVT = align256(kOffRotV + 4 * kHeadDim * kHeadDim);
+constexpr uint64_t kOffRotKT = align256(kOffRotVT + 4 * kHeadDim * kHeadDim);
+constexpr uint64_t kOffRows = align256(kOffRotKT + 4ull * kRotKFloats);
+__host__ __device__ constexpr uint64_t layout_total_bytes(int n_rows) {
+  return kOffRows + sizeof(RowMeta) * static_cast<uint64_t>(n_rows);
+}
+
+}  // namespace bgtq

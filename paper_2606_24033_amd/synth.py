@@ -130,3 +130,49 @@ def flat_rot_k(rot_k: dict, d_h: int = 128) -> np.ndarray:
 def ragged_lengths(seed: int, batch: int, lo: int, hi: int) -> np.ndarray:
     g = rng(seed, 0, 0, KIND_LENS)
     return g.integers(lo, hi + 1, size=batch).astype(np.int64)
+
+
+# --------------------------------------------------------------------------
+# Device-side generator for the long-context workloads (same recipe; the
+# stream is torch's CUDA generator seeded per (seed, layer, kind)).
+# --------------------------------------------------------------------------
+
+def torch_layer_kv(seed: int, layer: int, n: int, sigma: np.ndarray, base: float, t0: int = 0,
+                   device="cuda", dtype=None):
+    """Keys and values of every KV head of one layer for positions t0..t0+n-1.
+
+    sigma: [n_kv, 64] block profile.  Returns (k, v) [n, n_kv, 128] in `dtype`
+    (default bfloat16); keys rotary-embedded with float64 angles."""
+    import torch
+    dtype = torch.bfloat16 if dtype is None else dtype
+    n_kv = sigma.shape[0]
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) * 1000003 + int(layer) * 101 + 3)
+    z = torch.randn((n, n_kv, 128), generator=g, device=device, dtype=torch.float32)
+    sc = torch.from_numpy(np.concatenate([sigma, sigma], axis=1).astype(np.float32)).to(device)
+    k = z * sc[None]
+    k = _torch_rotary(k, torch.arange(t0, t0 + n, device=device, dtype=torch.float64), base)
+    g.manual_seed(int(seed) * 1000003 + int(layer) * 101 + 4)
+    v = torch.randn((n, n_kv, 128), generator=g, device=device, dtype=torch.float32)
+    return k.to(dtype), v.to(dtype)
+
+
+def torch_queries(seed: int, layer: int, n_q: int, pos, base: float, device="cuda", dtype=None):
+    """Decode queries [len(pos), n_q, 128] at positions `pos` (one per step)."""
+    import torch
+    dtype = torch.bfloat16 if dtype is None else dtype
+    pos = torch.as_tensor(pos, dtype=torch.float64, device=device)
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) * 1000003 + int(layer) * 101 + 5)
+    q = torch.randn((pos.numel(), n_q, 128), generator=g, device=device, dtype=torch.float32)
+    return _torch_rotary(q, pos, base).to(dtype)
+
+
+def _torch_rotary(x, pos, base):
+    import torch
+    inv = base ** (-2.0 * torch.arange(64, dtype=torch.float64, device=x.device) / 128)
+    ang = pos[:, None] * inv[None, :]
+    c = torch.cos(ang).to(torch.float32)[:, None, :]
+    s = torch.sin(ang).to(torch.float32)[:, None, :]
+    a, b = x[..., :64], x[..., 64:]
+    return torch.cat([a * c - b * s, a * s + b * c], dim=-1)

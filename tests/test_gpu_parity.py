@@ -1,0 +1,289 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 CPU oracle.
+
+Codes and norms: bit-exact except counted decision-boundary ties.
+Attention: max over (sequence, query head) of ||o_gpu - o_ref||_inf / ||o_ref||_inf <= 2e-3.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import blockgtq_oracle as o
+from paper_2606_24033_amd import synth
+from tests import _parity as P
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _require_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_24033_amd import blockgtq as bg
+    bg.lib()  # loud failure if the library is missing
+
+
+def bgm():
+    from paper_2606_24033_amd import blockgtq as bg
+    return bg
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(x, dtype):
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(device="cuda", dtype=torch.bfloat16 if dtype == "bf16" else torch.float32).contiguous()
+
+
+def build(st):
+    bg = bgm()
+    assert np.array_equal(st.bits, st.bits_oracle), "library and oracle allocations differ"
+    layout = bg.Layout(st.cfg, st.bits, synth.flat_rot_k(st.rot_k), st.rot_v)
+    cache = bg.Cache(st.cfg)
+    return layout, cache
+
+
+def append(st, layout, cache, layer, kv_list, write_pos):
+    """kv_list[seq][head] = (k [n,128], v [n,128]) -> one quantize_append call."""
+    bg = bgm()
+    B, H = st.cfg.batch, st.cfg.n_kv_heads
+    n = kv_list[0][0][0].shape[0]
+    K = np.zeros((B, n, H, 128), np.float32)
+    V = np.zeros((B, n, H, 128), np.float32)
+    for b in range(B):
+        for h in range(H):
+            K[b, :, h], V[b, :, h] = kv_list[b][h]
+    wp = torch.tensor(write_pos, dtype=torch.int32, device="cuda")
+    bg.blockgtq_quantize_append(st.cfg, layout, layer, to_dev(K, st.dtype), to_dev(V, st.dtype), wp, cache,
+                                host_write_pos=list(write_pos))
+
+
+def check_cache(st, cache, layer, seq, head, rows, T, stats, what):
+    bits = st.bits_oracle[layer, head]
+    widths = P.stream_widths(bits)
+    words = cache.k_codes[layer, seq, head, :T].cpu().numpy().view(np.uint32)
+    if not np.array_equal(words, rows.kwords[:T]):
+        P.compare_codes(P.read_fields(words, widths), rows.kcodes[:T], rows.kz[:T], widths, P.group_dims(bits),
+                        stats, what + " K")
+    else:
+        stats.codes += rows.kcodes[:T].size
+    ng = rows.knorms.shape[1]
+    kn = cache.k_norms[layer, seq, head, :ng, :T].cpu().numpy().T
+    P.compare_norms(kn, rows.knorms[:T], rows.kexact[:T], 128, stats, what + " K norms")
+    vt = cache.v_codes[layer, seq, head].cpu().numpy().view(np.uint32)
+    vc = P.read_value_codes(vt, st.cfg.v_bits, T)
+    P.compare_codes(vc, rows.vcodes[:T], rows.vz[:T], np.full(128, st.cfg.v_bits), np.full(128, 128), stats,
+                    what + " V")
+    vn = cache.v_norms[layer, seq, head, :T].cpu().numpy()
+    P.compare_norms(vn, rows.vnorms[:T], rows.vexact[:T], 128, stats, what + " V norms")
+
+
+def concat_rows(a, b):
+    return P.OracleRows(*[np.concatenate([x, y]) for x, y in zip(vars(a).values(), vars(b).values())])
+
+
+# ----------------------------------------------------------------------------
+
+def test_toy_single_head_end_to_end():
+    """1 layer, 1 KV head, G = 4, d_h = 128, base 1e4, 2048 fp32 rows, K3V2,
+    allocator on 256 calibration keys; append row 2048, attend 2049 rows."""
+    bg = bgm()
+    st = P.make_setup(1, 1, 1, 1, 4, 2080, 192, 2, 1e4, "fp32", n_cal=256)
+    layout, cache = build(st)
+    k, v = P.keys_values(st, 0, 0, 0, 2049)
+    append(st, layout, cache, 0, [[(k[:2048], v[:2048])]], [0])
+    append(st, layout, cache, 0, [[(k[2048:], v[2048:])]], [2048])
+    rows = P.oracle_rows(st, 0, 0, k, v)
+    stats = P.Stats()
+    check_cache(st, cache, 0, 0, 0, rows, 2049, stats, "toy")
+    log("toy ties", vars(stats))
+    q = synth.cast(synth.queries(1, 0, 0, 2048, 4, 1e4), "fp32")
+    ctx = torch.tensor([2049], dtype=torch.int32, device="cuda")
+    for ns in (0, 1, 5):
+        out = bg.blockgtq_decode_attn(st.cfg, layout, 0, to_dev(q[None], "fp32"), ctx, 2049, cache, n_splits=ns)
+        ref = P.oracle_attention(st, 0, 0, q, rows, 2049)
+        err = P.rel_err(out[0].cpu().numpy().astype(np.float64), ref)
+        log("toy n_splits", ns, "rel err", err)
+        assert err <= 2e-3
+    # fp16 comparator against the definition on fp16-rounded K/V
+    k16 = torch.zeros((1, 1, 1, 2080, 128), dtype=torch.float16, device="cuda")
+    v16 = torch.zeros_like(k16)
+    k16[0, 0, 0, :2049] = torch.from_numpy(k.astype(np.float32)).half().cuda()
+    v16[0, 0, 0, :2049] = torch.from_numpy(v.astype(np.float32)).half().cuda()
+    out16 = bg.blockgtq_decode_attn_fp16(st.cfg, 0, to_dev(q[None], "fp32"), ctx, 2049, k16, v16)
+    ref16 = o.attention(q, k.astype(np.float16).astype(np.float64), v.astype(np.float16).astype(np.float64))
+    assert P.rel_err(out16[0].cpu().numpy().astype(np.float64), ref16) <= 2e-3
+    assert stats.code_ties <= 1e-4 * stats.codes
+
+
+def test_qwen_shaped_layer_prefill_then_decode_steps():
+    """Qwen2.5-3B attention shape: 16 query heads, 2 KV heads, base 1e6, bf16,
+    K3V3; prefill-quantize 32768 rows in one call, then decode steps that each
+    append one row and attend over the whole cache."""
+    bg = bgm()
+    T, steps = 32768, 4
+    st = P.make_setup(2, 1, 1, 2, 8, T + 64, 192, 3, 1e6, "bf16", n_cal=2048)
+    layout, cache = build(st)
+    kv = [P.keys_values(st, 0, h, 0, T + steps) for h in range(2)]
+    append(st, layout, cache, 0, [[(kv[h][0][:T], kv[h][1][:T]) for h in range(2)]], [0])
+    rows = [P.oracle_rows(st, 0, h, kv[h][0], kv[h][1]) for h in range(2)]
+    stats = P.Stats()
+    for h in range(2):
+        check_cache(st, cache, 0, 0, h, rows[h], T, stats, f"qwen prefill h{h}")
+    log("qwen prefill ties", vars(stats))
+    for s in range(steps):
+        pos = T + s
+        append(st, layout, cache, 0, [[(kv[h][0][pos:pos + 1], kv[h][1][pos:pos + 1]) for h in range(2)]], [pos])
+        q = np.concatenate([synth.cast(synth.queries(2, 0, h, pos, 8, 1e6, step=s), "bf16") for h in range(2)])
+        ctx = torch.tensor([pos + 1], dtype=torch.int32, device="cuda")
+        out = bg.blockgtq_decode_attn(st.cfg, layout, 0, to_dev(q[None], "bf16"), ctx, pos + 1, cache)
+        out = out[0].cpu().numpy().astype(np.float64)
+        for h in range(2):
+            ref = P.oracle_attention(st, 0, h, q[h * 8:(h + 1) * 8], rows[h], pos + 1)
+            err = P.rel_err(out[h * 8:(h + 1) * 8], ref)
+            log("qwen step", s, "head", h, "rel err", err)
+            assert err <= 2e-3
+    for h in range(2):
+        check_cache(st, cache, 0, 0, h, rows[h], T + steps, stats, f"qwen final h{h}")
+    assert stats.code_ties <= 1e-4 * stats.codes
+
+
+def test_ragged_batch_unaligned_appends_and_edge_lengths():
+    """Batch of 4 with different lengths, appends at positions that are not
+    tile-aligned (value tiles are read-modify-written), a zero-length context,
+    a one-row context, and an exactly-full tile."""
+    bg = bgm()
+    st = P.make_setup(4, 1, 4, 2, 4, 512, 192, 2, 5e5, "bf16", n_cal=256)
+    layout, cache = build(st)
+    starts = [0, 37, 300, 5]
+    n1, n2 = 27, 9
+    p0 = max(starts)
+    allkv = {(b, h): P.keys_values(st, 0, h, 1000 * b, starts[b] + n1 + n2) for b in range(4) for h in range(2)}
+    junk_k, junk_v = P.keys_values(st, 0, 1, 99999, p0)
+    # one prefill call for every sequence: real rows below its start, other rows beyond
+    pre = [[(np.concatenate([allkv[b, h][0][:starts[b]], junk_k[starts[b]:]]),
+             np.concatenate([allkv[b, h][1][:starts[b]], junk_v[starts[b]:]])) for h in range(2)] for b in range(4)]
+    append(st, layout, cache, 0, pre, [0] * 4)
+    pos = list(starts)
+    for n in (n1, n2):
+        kvb = [[(allkv[b, h][0][pos[b]:pos[b] + n], allkv[b, h][1][pos[b]:pos[b] + n]) for h in range(2)]
+               for b in range(4)]
+        append(st, layout, cache, 0, kvb, pos)
+        pos = [p + n for p in pos]
+    stats = P.Stats()
+    rows = {}
+    for b in range(4):
+        for h in range(2):
+            rows[b, h] = P.oracle_rows(st, 0, h, allkv[b, h][0], allkv[b, h][1])
+            check_cache(st, cache, 0, b, h, rows[b, h], pos[b], stats, f"ragged b{b} h{h}")
+    log("ragged ties", vars(stats))
+    ctx_cases = [[0, 1, 32, pos[3]], pos, [pos[0], 64, 33, 1]]
+    for ctxl in ctx_cases:
+        q = np.stack([np.concatenate([synth.cast(synth.queries(4, b, h, 0, 4, 5e5), "bf16") for h in range(2)])
+                      for b in range(4)])
+        ctx = torch.tensor(ctxl, dtype=torch.int32, device="cuda")
+        for ns in (0, 3):
+            out = bg.blockgtq_decode_attn(st.cfg, layout, 0, to_dev(q, "bf16"), ctx, max(ctxl), cache,
+                                          n_splits=ns).cpu().numpy().astype(np.float64)
+            for b in range(4):
+                for h in range(2):
+                    got = out[b, h * 4:(h + 1) * 4]
+                    if ctxl[b] == 0:
+                        assert np.all(got == 0)
+                        continue
+                    ref = P.oracle_attention(st, 0, h, q[b, h * 4:(h + 1) * 4], rows[b, h], ctxl[b])
+                    assert P.rel_err(got, ref) <= 2e-3, (ctxl, b, h)
+
+
+def test_all_layers_launch_matches_per_layer_and_split_invariance():
+    bg = bgm()
+    st = P.make_setup(5, 3, 2, 2, 4, 1024, 128, 2, 1e4, "bf16", n_cal=128)
+    layout, c1 = build(st)
+    c2 = bg.Cache(st.cfg)
+    T = 700
+    K = np.zeros((3, 2, T, 2, 128), np.float32)
+    V = np.zeros_like(K)
+    for layer in range(3):
+        for b in range(2):
+            for h in range(2):
+                K[layer, b, :, h], V[layer, b, :, h] = P.keys_values(st, layer, h, 5000 * b, T)
+    wp = torch.zeros(2, dtype=torch.int32, device="cuda")
+    for layer in range(3):
+        bg.blockgtq_quantize_append(st.cfg, layout, layer, to_dev(K[layer], "bf16"), to_dev(V[layer], "bf16"), wp, c1)
+    bg.blockgtq_quantize_append(st.cfg, layout, -1, to_dev(K, "bf16"), to_dev(V, "bf16"), wp, c2)
+    for a, b in zip((c1.k_codes, c1.k_norms, c1.v_codes, c1.v_norms), (c2.k_codes, c2.k_norms, c2.v_codes, c2.v_norms)):
+        assert torch.equal(a, b)
+    g = np.random.default_rng(0)
+    Q = synth.cast(g.standard_normal((3, 2, 8, 128)), "bf16")
+    ctx = torch.tensor([T, 411], dtype=torch.int32, device="cuda")
+    outs = {}
+    for ns in (1, 2, 7, 22, 0):
+        outs[ns] = bg.blockgtq_decode_attn(st.cfg, layout, -1, to_dev(Q, "bf16"), ctx, T, c1, n_splits=ns)
+        per = torch.stack([bg.blockgtq_decode_attn(st.cfg, layout, layer, to_dev(Q[layer], "bf16"), ctx, T, c1,
+                                                   n_splits=ns) for layer in range(3)])
+        assert torch.equal(per, outs[ns])
+    for ns in (2, 7, 22, 0):
+        rel = (outs[ns] - outs[1]).abs().max() / outs[1].abs().max()
+        assert rel <= 1e-5
+    again = bg.blockgtq_decode_attn(st.cfg, layout, -1, to_dev(Q, "bf16"), ctx, T, c1, n_splits=7)
+    assert torch.equal(again, outs[7])
+    # oracle check for a few (layer, seq, head)
+    for layer, b, h in ((0, 0, 0), (2, 1, 1), (1, 1, 0)):
+        rows = P.oracle_rows(st, layer, h, K[layer, b, :, h], V[layer, b, :, h])
+        ctxl = int(ctx[b])
+        ref = P.oracle_attention(st, layer, h, Q[layer, b, h * 4:(h + 1) * 4], rows, ctxl)
+        assert P.rel_err(outs[0][layer, b, h * 4:(h + 1) * 4].cpu().numpy().astype(np.float64), ref) <= 2e-3
+
+
+def test_zero_rows_and_noop_calls():
+    bg = bgm()
+    st = P.make_setup(6, 1, 1, 1, 2, 64, 160, 4, 1e4, "fp32", n_cal=64)
+    layout, cache = build(st)
+    k, v = P.keys_values(st, 0, 0, 0, 40)
+    k[3] = 0.0
+    v[5] = 0.0
+    k[7, :64] = 0.0
+    k[7, 64:] = 0.0
+    append(st, layout, cache, 0, [[(k, v)]], [0])
+    rows = P.oracle_rows(st, 0, 0, k, v)
+    stats = P.Stats()
+    check_cache(st, cache, 0, 0, 0, rows, 40, stats, "zero rows")
+    assert np.all(cache.v_norms[0, 0, 0, 5].cpu().numpy() == 0)
+    # n_new == 0 is a no-op
+    before = cache.k_codes.clone()
+    bg.blockgtq_quantize_append(st.cfg, layout, 0, to_dev(np.zeros((1, 0, 1, 128)), "fp32"),
+                                to_dev(np.zeros((1, 0, 1, 128)), "fp32"),
+                                torch.zeros(1, dtype=torch.int32, device="cuda"), cache)
+    torch.cuda.synchronize()
+    assert torch.equal(before, cache.k_codes)
+    q = synth.cast(synth.queries(6, 0, 0, 40, 2, 1e4), "fp32")
+    ctx = torch.tensor([40], dtype=torch.int32, device="cuda")
+    out = bg.blockgtq_decode_attn(st.cfg, layout, 0, to_dev(q[None], "fp32"), ctx, 40, cache)
+    ref = P.oracle_attention(st, 0, 0, q, rows, 40)
+    assert P.rel_err(out[0].cpu().numpy().astype(np.float64), ref) <= 2e-3
+
+
+def test_argument_errors_on_device():
+    bg = bgm()
+    st = P.make_setup(7, 1, 1, 1, 4, 64, 192, 3, 1e4, "fp32", n_cal=32)
+    layout, cache = build(st)
+    q = to_dev(np.zeros((1, 4, 128)), "fp32")
+    ctx = torch.tensor([10], dtype=torch.int32, device="cuda")
+    small = torch.empty(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(bg.BlockGTQError) as e:
+        bg.blockgtq_decode_attn(st.cfg, layout, 0, q, ctx, 10, cache, workspace=small)
+    assert e.value.code == -4
+    with pytest.raises(bg.BlockGTQError) as e:
+        bg.blockgtq_decode_attn(st.cfg, layout, 0, q, ctx, 65, cache)
+    assert e.value.code == -3
+    with pytest.raises(bg.BlockGTQError):
+        bg.blockgtq_decode_attn(st.cfg, layout, 1, q, ctx, 10, cache)
+    with pytest.raises(bg.BlockGTQError):
+        bad = np.array(st.bits)
+        bad[0, 0, 0] += 1
+        bg.Layout(st.cfg, bad, synth.flat_rot_k(st.rot_k), st.rot_v)

@@ -1,0 +1,92 @@
+"""CPU tests of the C ABI: symbols, host-side method steps against the oracle,
+and argument errors.  No device call is made here."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import blockgtq_oracle as o
+from paper_2606_24033_amd import blockgtq as bg
+from paper_2606_24033_amd import synth
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "blockgtq.h")
+
+
+def test_library_exports_every_declared_symbol():
+    names = set(re.findall(r"\b(blockgtq_\w+)\s*\(", open(HEADER).read()))
+    assert names == set(bg.EXPORTED)
+    L = ctypes.CDLL(bg.LIB_PATH)
+    for n in names:
+        assert getattr(L, n) is not None
+
+
+@pytest.mark.parametrize("b", range(1, 9))
+def test_codebook_bit_exact_vs_oracle(b):
+    c16, thr = bg.blockgtq_codebook(b)
+    oc, ot = o.codebook(b)
+    np.testing.assert_array_equal(c16.astype(np.float64), oc)
+    np.testing.assert_array_equal(thr.astype(np.float64), ot)
+
+
+def test_energy_scores_vs_oracle():
+    sig = synth.sigma_profile(1, 0, 0)
+    q, k = synth.calibration(1, 0, 0, 256, 4, sig)
+    q, k = q.astype(np.float32), k.astype(np.float32)
+    np.testing.assert_allclose(bg.blockgtq_energy_scores(q, k), o.energy_scores(q, k), rtol=1e-13)
+
+
+def test_allocator_bit_exact_vs_oracle():
+    g = np.random.default_rng(3)
+    rows = [np.exp(2 * g.standard_normal(64)) for _ in range(40)]
+    rows += [np.ones(64), np.zeros(64), np.array([4.0 ** (i % 5) for i in range(64)]),
+             np.repeat([1.0, 16.0], 32), np.array([0.0] * 63 + [1.0])]
+    s = np.stack(rows)
+    for budget in (64, 100, 128, 192, 256, 511, 512):
+        got = bg.blockgtq_allocate(s, budget)
+        for r in range(len(rows)):
+            np.testing.assert_array_equal(got[r], o.allocate(s[r], budget))
+
+
+def test_allocator_small_blocks_and_bounds():
+    g = np.random.default_rng(8)
+    for _ in range(50):
+        s = np.exp(g.standard_normal(4))
+        for B in range(4, 33):
+            np.testing.assert_array_equal(bg.blockgtq_allocate(s, B, 1, 8)[0], o.allocate(s, B, 1, 8))
+        for B in range(8, 17):
+            np.testing.assert_array_equal(bg.blockgtq_allocate(s, B, 2, 4)[0], o.allocate(s, B, 2, 4))
+
+
+def test_allocator_errors():
+    s = np.ones((1, 64))
+    with pytest.raises(bg.BlockGTQError) as e:
+        bg.blockgtq_allocate(s, 63)
+    assert e.value.code == -2
+    with pytest.raises(bg.BlockGTQError) as e:
+        bg.blockgtq_allocate(-s, 128)
+    assert e.value.code == -1
+    with pytest.raises(bg.BlockGTQError):
+        bg.blockgtq_allocate(s * np.nan, 128)
+    with pytest.raises(bg.BlockGTQError):
+        bg.blockgtq_allocate(s, 128, 0, 8)
+
+
+def test_sizes_and_config_errors():
+    cfg = bg.Config(n_layers=32, batch=1, n_kv_heads=8, group=4, capacity=131072 + 64, k_budget=128, v_bits=2)
+    kc, kn, vc, vn = bg.cache_bytes(cfg)
+    rows = 32 * 8 * cfg.capacity
+    assert kc == rows * 32 and vc == rows * 32 and vn == rows * 2 and kn == rows * 16
+    ws = bg.workspace_bytes(cfg, 32, 0, 131072)
+    assert ws > 0
+    bad = bg.Config(n_layers=1, batch=1, n_kv_heads=1, group=4, capacity=100, k_budget=128, v_bits=2)
+    with pytest.raises(bg.BlockGTQError):
+        bg.cache_bytes(bad)
+    bad = bg.Config(n_layers=1, batch=1, n_kv_heads=1, group=9, capacity=128, k_budget=128, v_bits=2)
+    with pytest.raises(bg.BlockGTQError) as e:
+        bg.cache_bytes(bad)
+    assert e.value.code == -5
+    with pytest.raises(bg.BlockGTQError) as e:
+        bg.workspace_bytes(cfg, 32, 0, cfg.capacity + 1)
+    assert e.value.code == -3
