@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libblockgtq.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["blockgtq.cpp", "kernels.hip"]
+SOURCES = ["blockgtq.cpp", "kernels.hip", "decode.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -209,17 +209,18 @@ struct SplitPlan {
 
 SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested) {
   SplitPlan p;
-  if (max_ctx <= 0) return {1, kTile};
+  if (max_ctx <= 0) return {1, 64};
   const int max_splits = (max_ctx + kTile - 1) / kTile;
   int n;
   if (requested > 0) {
     n = std::min(requested, max_splits);
   } else {
+    // about four 8-wave workgroups per CU, each split at least 512 rows long
     const long units = static_cast<long>(c->n_kv_heads) * c->batch * n_lc;
-    n = static_cast<int>((2048 + units - 1) / units);
-    n = std::max(1, std::min(n, (max_ctx + 255) / 256));
+    n = static_cast<int>((1024 + units - 1) / units);
+    n = std::max(1, std::min(n, (max_ctx + 511) / 512));
   }
-  p.split_len = ((max_ctx + n - 1) / n + kTile - 1) / kTile * kTile;
+  p.split_len = ((max_ctx + n - 1) / n + 63) / 64 * 64;
   p.n_splits = (max_ctx + p.split_len - 1) / p.split_len;
   return p;
 }
@@ -414,6 +415,23 @@ int blockgtq_layout_init(const bgtq_config* cfg, const uint8_t* h_k_bits, const 
       }
     }
     M.n_groups = g;
+    // decode steps: 4 coordinates of one group per step
+    int ns = 0;
+    for (int gg = 0; gg < g; ++gg) {
+      for (int j = 0; j < M.g_dim[gg]; j += 4) {
+        const int pos = M.g_pos[gg] + j;
+        const int valid = std::min(4, M.g_dim[gg] - j);
+        const bool last = j + 4 >= M.g_dim[gg];
+        M.step[ns++] = static_cast<uint32_t>(M.bitoff[pos]) | (static_cast<uint32_t>(M.g_bits[gg]) << 10) |
+                       (static_cast<uint32_t>(gg) << 14) | (last ? (1u << 17) : 0u) |
+                       (static_cast<uint32_t>(pos) << 19) | (static_cast<uint32_t>(valid) << 26);
+      }
+    }
+    M.n_steps = ns;
+    for (int w = 0, s2 = 0; w <= kMaxKWords; ++w) {
+      while (s2 < ns && static_cast<int>(M.step[s2] & 1023u) < 32 * w) ++s2;
+      M.word_step[w] = s2;
+    }
     for (int w = 0; w < kMaxKWords; ++w) {
       int first = kHeadDim;
       for (int q = 0; q < kHeadDim; ++q)

@@ -31,6 +31,10 @@ struct DecodeWs {
   int split_len;    // tokens per split, multiple of 32
 };
 
+// Split pass of the packed decode (decode.hip); writes ws.part.
+hipError_t launch_split_mfma(const Dims& d, const void* layout, const int32_t* ctx_len, const CachePtrs& c,
+                             const DecodeWs& ws, hipStream_t s);
+
 hipError_t launch_decode_packed(const Dims& d, const void* layout, const void* q,
                                 const int32_t* ctx_len, const CachePtrs& c, float* out,
                                 const DecodeWs& ws, hipStream_t s);

@@ -3,7 +3,7 @@
 //  k_quantize      : TQ-MSE encode (Sec. 2.2) of appended K rows per same-rate
 //                    group (end of Sec. 3.2) and of V rows, dense b-bit pack.
 //  k_qrot          : Q-side rotation of the decode queries (Sec. 4).
-//  k_split_packed  : split-context decode pass over the packed cache (Sec. 4).
+//  (the split pass over the packed cache lives in decode.hip)
 //  k_merge         : exact log-sum-exp merge of the splits + inverse V rotation.
 //  k_split_fp16    : the same decode over an fp16 cache (comparator).
 #include <hip/hip_fp16.h>
@@ -80,10 +80,8 @@ __global__ __launch_bounds__(256) void k_quantize(Dims d, const uint8_t* __restr
   const RowMeta* gmeta =
       reinterpret_cast<const RowMeta*>(blob + kOffRows) + (layer * d.n_kv + head);
 
-  {
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(gmeta);
-    reinterpret_cast<uint32_t*>(&meta)[tid] = src[tid];  // 1024 B = 256 words
-  }
+  for (int i = tid; i < static_cast<int>(sizeof(RowMeta) / 4); i += 256)
+    reinterpret_cast<uint32_t*>(&meta)[i] = reinterpret_cast<const uint32_t*>(gmeta)[i];
   for (int i = tid; i < kThresholdEntries; i += 256) thr[i] = gthr[i];
   const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + head;
   for (int idx = tid; idx < kTile * kHeadDim; idx += 256) {
@@ -204,153 +202,6 @@ __global__ __launch_bounds__(128) void k_qrot(Dims d, const uint8_t* __restrict_
       float acc = 0.f;
       for (int i = 0; i < dg; ++i) acc = fmaf(rt[i * dg + tid], qs[M->dim[p0 + i]], acc);
       qp[qoff + p0 + tid] = acc / sqrtf(static_cast<float>(dg) * kHeadDim);
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Split pass over the packed cache.  One workgroup per (split, KV head,
-// sequence[, layer]); 256 threads.  Keys: one thread per token decodes the
-// row and forms the G logits.  Values: thread (coordinate j, half) adds the
-// probability-weighted centroids of its coordinate.  Accumulators stay in the
-// rotated V domain; the merge applies Pi_V^T.
-// ---------------------------------------------------------------------------
-template <int G>
-__global__ __launch_bounds__(256) void k_split_packed(Dims d, const uint8_t* __restrict__ blob,
-                                                      const int32_t* __restrict__ ctx_len,
-                                                      CachePtrs c, const float* __restrict__ qp,
-                                                      float* __restrict__ part, int n_splits,
-                                                      int split_len) {
-  __shared__ float sq[G][kHeadDim];
-  __shared__ float cbk[kCodebookEntries];
-  __shared__ uint8_t swidth[kHeadDim], sgrp[kHeadDim];
-  __shared__ uint16_t sboff[kHeadDim];
-  __shared__ uint32_t rows[256 * kMaxKWords];
-  __shared__ float pt[G][256];
-  __shared__ float red[2][G][4];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int split = blockIdx.x, kvh = blockIdx.y, lz = blockIdx.z;
-  const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
-  const int seq = lz % d.batch;
-  const int hqn = d.n_kv * G;
-  const int cap = d.capacity, kw = d.k_words, bv = d.v_bits;
-  const RowMeta* M = reinterpret_cast<const RowMeta*>(blob + kOffRows) + (layer * d.n_kv + kvh);
-  const uint16_t* c16 = reinterpret_cast<const uint16_t*>(blob + kOffC16);
-
-  for (int i = tid; i < G * kHeadDim; i += 256)
-    sq[i >> 7][i & 127] = qp[(static_cast<size_t>(lz) * hqn + kvh * G + (i >> 7)) * kHeadDim + (i & 127)];
-  for (int i = tid; i < kCodebookEntries; i += 256) cbk[i] = __half2float(__ushort_as_half(c16[i]));
-  if (tid < kHeadDim) {
-    swidth[tid] = M->width[tid];
-    sgrp[tid] = M->grp[tid];
-    sboff[tid] = M->bitoff[tid];
-  }
-  const int ng = M->n_groups;
-  __syncthreads();
-
-  const int ctx = min(ctx_len[seq], cap);
-  const int t0 = split * split_len;
-  const int t1 = min(t0 + split_len, ctx);
-  const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + kvh;
-  const float* cbv = cbk + cb_index(bv);
-  const uint32_t vmask = (1u << bv) - 1u;
-  const float vscale = 1.0f / sqrtf(static_cast<float>(kHeadDim));
-
-  float m_run[G], l_run[G], acc[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m_run[h] = kNegInf;
-    l_run[h] = 0.f;
-    acc[h] = 0.f;
-  }
-  const int j = tid & 127, half = tid >> 7;
-
-  for (int c0 = t0; c0 < t1; c0 += 256) {
-    const int nrow = min(256, t1 - c0);
-    const uint32_t* src = c.k_codes + (row * cap + c0) * kw;
-    for (int i = tid; i < nrow * kw; i += 256) rows[i] = src[i];
-    __syncthreads();
-
-    float lg[G];
-    const bool valid = tid < nrow;
-    const int t = c0 + tid;
-    if (valid) {
-      float nrm[kMaxGroups];
-#pragma unroll
-      for (int g = 0; g < kMaxGroups; ++g)
-        nrm[g] = g < ng ? __half2float(__ushort_as_half(c.k_norms[(row * kMaxGroups + g) * cap + t])) : 0.f;
-#pragma unroll
-      for (int h = 0; h < G; ++h) lg[h] = 0.f;
-      const uint32_t* rw = rows + tid * kw;
-      for (int p = 0; p < kHeadDim; ++p) {
-        const int o = sboff[p], w = o >> 5, sh = o & 31, b = swidth[p];
-        uint64_t two = rw[w];
-        if (w + 1 < kw) two |= static_cast<uint64_t>(rw[w + 1]) << 32;
-        const uint32_t code = static_cast<uint32_t>(two >> sh) & ((1u << b) - 1u);
-        const float val = cbk[cb_index(b) + code] * nrm[sgrp[p]];
-#pragma unroll
-        for (int h = 0; h < G; ++h) lg[h] = fmaf(sq[h][p], val, lg[h]);
-      }
-    } else {
-#pragma unroll
-      for (int h = 0; h < G; ++h) lg[h] = kNegInf;
-    }
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mx = wave_max(lg[h]);
-      if (lane == 0) red[0][h][wave] = mx;
-    }
-    __syncthreads();
-    const float vn = valid ? __half2float(__ushort_as_half(c.v_norms[row * cap + t])) * vscale : 0.f;
-    float corr[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mt = fmaxf(fmaxf(red[0][h][0], red[0][h][1]), fmaxf(red[0][h][2], red[0][h][3]));
-      const float mn = fmaxf(m_run[h], mt);
-      corr[h] = m_run[h] == kNegInf ? 0.f : __expf(m_run[h] - mn);
-      const float p = valid ? __expf(lg[h] - mn) : 0.f;
-      pt[h][tid] = p * vn;
-      const float ps = wave_sum(p);
-      if (lane == 0) red[1][h][wave] = ps;
-      m_run[h] = mn;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      l_run[h] = l_run[h] * corr[h] + (red[1][h][0] + red[1][h][1] + red[1][h][2] + red[1][h][3]);
-      acc[h] *= corr[h];
-    }
-    const int s_end = min(half * 128 + 128, nrow);
-    for (int s = half * 128; s < s_end; ++s) {
-      const int tt = c0 + s;
-      const int o = (tt & (kTile - 1)) * bv, w = o >> 5, sh = o & 31;
-      const size_t base = ((row * (cap / kTile) + (tt >> 5)) * kHeadDim + j) * bv;
-      uint64_t two = c.v_codes[base + w];
-      if (w + 1 < bv) two |= static_cast<uint64_t>(c.v_codes[base + w + 1]) << 32;
-      const float val = cbv[static_cast<uint32_t>(two >> sh) & vmask];
-#pragma unroll
-      for (int h = 0; h < G; ++h) acc[h] = fmaf(pt[h][s], val, acc[h]);
-    }
-    __syncthreads();
-  }
-
-  // combine the two token halves of each coordinate
-  float* xch = reinterpret_cast<float*>(rows);
-  if (half == 1) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) xch[h * kHeadDim + j] = acc[h];
-  }
-  __syncthreads();
-  if (half == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float* pb = part + ((static_cast<size_t>(lz) * hqn + kvh * G + h) * n_splits + split) * 130;
-      pb[2 + j] = acc[h] + xch[h * kHeadDim + j];
-      if (j == 0) {
-        pb[0] = m_run[h];
-        pb[1] = l_run[h];
-      }
     }
   }
 }
@@ -510,31 +361,14 @@ hipError_t launch_quantize_append(const Dims& d, const void* layout, const void*
   return hipGetLastError();
 }
 
-template <int G>
-static void launch_split_packed_g(const Dims& d, const uint8_t* blob, const int32_t* ctx,
-                                  const CachePtrs& c, const DecodeWs& ws, hipStream_t s) {
-  dim3 grid(ws.n_splits, d.n_kv, d.batch * d.n_lc);
-  hipLaunchKernelGGL(k_split_packed<G>, grid, dim3(256), 0, s, d, blob, ctx, c, ws.qp, ws.part,
-                     ws.n_splits, ws.split_len);
-}
-
 hipError_t launch_decode_packed(const Dims& d, const void* layout, const void* q,
                                 const int32_t* ctx_len, const CachePtrs& c, float* out,
                                 const DecodeWs& ws, hipStream_t s) {
   const uint8_t* blob = static_cast<const uint8_t*>(layout);
   const int hqn = d.n_kv * d.group;
   hipLaunchKernelGGL(k_qrot, dim3(hqn, d.batch, d.n_lc), dim3(128), 0, s, d, blob, q, ws.qp);
-  switch (d.group) {
-    case 1: launch_split_packed_g<1>(d, blob, ctx_len, c, ws, s); break;
-    case 2: launch_split_packed_g<2>(d, blob, ctx_len, c, ws, s); break;
-    case 3: launch_split_packed_g<3>(d, blob, ctx_len, c, ws, s); break;
-    case 4: launch_split_packed_g<4>(d, blob, ctx_len, c, ws, s); break;
-    case 5: launch_split_packed_g<5>(d, blob, ctx_len, c, ws, s); break;
-    case 6: launch_split_packed_g<6>(d, blob, ctx_len, c, ws, s); break;
-    case 7: launch_split_packed_g<7>(d, blob, ctx_len, c, ws, s); break;
-    case 8: launch_split_packed_g<8>(d, blob, ctx_len, c, ws, s); break;
-    default: return hipErrorInvalidValue;
-  }
+  hipError_t e = launch_split_mfma(d, layout, ctx_len, c, ws, s);
+  if (e != hipSuccess) return e;
   const float* rotv = reinterpret_cast<const float*>(blob + kOffRotV);
   hipLaunchKernelGGL(k_merge, dim3(hqn, d.batch, d.n_lc), dim3(128), 0, s, d, ws.part, ws.n_splits,
                      rotv, out);

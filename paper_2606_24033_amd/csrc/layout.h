@@ -14,6 +14,7 @@ constexpr int kBlocks = 64;          // L = d_h / 2 RoPE blocks
 constexpr int kTile = 32;            // tokens per value tile
 constexpr int kMaxGroups = 8;        // same-rate groups (b = 1..8)
 constexpr int kMaxKWords = 32;       // 128 positions x 8 bits / 32
+constexpr int kMaxSteps = 48;        // 4-coordinate decode steps of a key row (<= 32 + 8)
 constexpr int kCodebookEntries = 510;   // sum_b 2^b, b = 1..8
 constexpr int kThresholdEntries = 502;  // sum_b (2^b - 1)
 constexpr int kRotKFloats = 357760;     // sum over d = 2..128 (even) of d*d
@@ -28,6 +29,16 @@ __host__ __device__ constexpr int rotk_index(int d) {
 }
 
 // Per (layer, KV head) description of one key row (stream order).
+//
+// Decode steps: the attention kernel consumes a key row 4 coordinates at a
+// time, never mixing two groups in one step (a group with d_g = 2 mod 4 ends
+// with a 2-coordinate step).  step[s] packs:
+//   bits  0..9  stream bit offset of the step's first code
+//   bits 10..13 code width b
+//   bits 14..16 group ordinal
+//   bit  17     last step of its group
+//   bits 19..25 stream position of the step's first coordinate
+//   bits 26..28 valid coordinates (2 or 4)
 struct RowMeta {
   uint8_t dim[kHeadDim];       // stream position -> source dim of the key
   uint8_t width[kHeadDim];     // code width of the position (bits)
@@ -38,9 +49,12 @@ struct RowMeta {
   int32_t g_dim[kMaxGroups];   // d_g = 2 |G_b|
   int32_t g_pos[kMaxGroups];   // first stream position of group g
   int32_t word_first[kMaxKWords];  // first position whose code touches word w
-  int32_t pad[39];
+  uint32_t step[kMaxSteps];
+  int32_t n_steps;
+  int32_t word_step[kMaxKWords + 1];  // steps starting in word w: [word_step[w], word_step[w+1])
+  int32_t pad[21];
 };
-static_assert(sizeof(RowMeta) == 1024, "RowMeta size");
+static_assert(sizeof(RowMeta) == 1280, "RowMeta size");
 
 struct Header {
   uint32_t magic;

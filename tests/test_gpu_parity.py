@@ -227,9 +227,12 @@ def test_all_layers_launch_matches_per_layer_and_split_invariance():
         per = torch.stack([bg.blockgtq_decode_attn(st.cfg, layout, layer, to_dev(Q[layer], "bf16"), ctx, T, c1,
                                                    n_splits=ns) for layer in range(3)])
         assert torch.equal(per, outs[ns])
+    # Probabilities enter the PV product as fp16, rounded after subtracting
+    # the running max of each split, so two partitions may differ by one fp16
+    # rounding of every weight: at most 2^-11 relative.
     for ns in (2, 7, 22, 0):
         rel = (outs[ns] - outs[1]).abs().max() / outs[1].abs().max()
-        assert rel <= 1e-5
+        assert rel <= 1e-3
     again = bg.blockgtq_decode_attn(st.cfg, layout, -1, to_dev(Q, "bf16"), ctx, T, c1, n_splits=7)
     assert torch.equal(again, outs[7])
     # oracle check for a few (layer, seq, head)
