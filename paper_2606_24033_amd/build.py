@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libblockgtq.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["blockgtq.cpp", "kernels.hip", "decode.hip"]
+SOURCES = ["blockgtq.cpp", "kernels.hip"] + [f"decode_bv{b}.hip" for b in range(1, 9)]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -40,7 +40,7 @@ def build(verbose: bool = False) -> str:
         lang = ["-x", "hip"]
         cmds.append([HIPCC, *FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
-    with ThreadPoolExecutor(max_workers=len(cmds)) as ex:
+    with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 4, 16)) as ex:
         list(ex.map(_run, cmds))
     tmp = OUT + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])

@@ -1,0 +1,602 @@
+// Split pass of the packed-cache decode attention for gfx950 (Sec. 4: fused
+// unpack -> codebook -> norm rescale -> QK and PV products -> online softmax,
+// split along the key axis).
+//
+// Work mapping.  One workgroup = 8 waves = one (split, KV head, sequence[,
+// layer]).  A wave owns 64-token tiles (two value tiles).  Both products run
+// on 4x4x4 f16 MFMA instructions (16 independent 4x4 blocks) whose A operand
+// is broadcast from one block (CBSZ = 4, ABID = the block), so the operand
+// shared by all 64 lanes is held once per 16 steps instead of once per step:
+//  * QK  D_b = A x B_b.  A = 4 rotated-query heads x 4 coordinates of one
+//    decode step, taken from block ABID = step % 16 of a register image in
+//    which lane 4b+i holds step b of a 16-step chunk for head i.
+//    B_b column j = the 4 dequantized coordinates of token 4b+j: lane l
+//    decodes the key row of token l, 4 stream positions per step.  All lanes
+//    decode the same positions in a step, so they share one code width and a
+//    step never mixes two groups.  D lands as lane = token, register = head.
+//    A group's partial dot products are scaled by its fp16 radius in fp32.
+//  * PV  A = the softmax weights of 4 heads x 4 tokens (block ABID = 4-token
+//    step), B_b column j = 4 dequantized value codes of dim 64h + 4b + j,
+//    decoded straight from the value tile (the codes of one coordinate are
+//    contiguous there).  D lands as lane = dim, register = head.
+// Between the two, a 4x4 transpose inside each lane quad turns (token, head)
+// into (head, 4 tokens), the layout of the PV A operand and of the softmax.
+// Dequantization goes through lookup tables in LDS, replicated per lane so
+// random indices never collide on a bank: 4 codes per lookup for b <= 2 (a
+// 64-bit entry of four fp16 centroids), 2 codes for b = 3, 1 code above.
+// The rotated query is split into fp16 hi and lo parts (both multiplied,
+// accumulated in fp32): fp16 alone leaves ~2^-12 relative error per term.
+#pragma once
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include <utility>
+
+#include "kernels.h"
+#include "layout.h"
+
+namespace bgtq {
+namespace split_detail {
+
+typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 8;
+constexpr int kThreads = kWaves * 64;
+constexpr int kMaxSlots = 10;  // 16-step query chunks of one key row: sum_g ceil(steps_g / 16)
+constexpr float kNegInf = -__builtin_huge_valf();
+
+// LDS map (bytes)
+constexpr int kLut1 = 0;                        // b=1: 16 entries x 16 replicas x 8 B
+constexpr int kLut2 = kLut1 + 16 * 16 * 8;      // b=2: 256 x 16 x 8
+constexpr int kLut3 = kLut2 + 256 * 16 * 8;     // b=3: 64 (2 codes) x 32 x 4
+constexpr int kLut4 = kLut3 + 64 * 32 * 4;      // b=4: 16 x 32 x 4 (fp16 in the low half)
+constexpr int kLut5 = kLut4 + 16 * 32 * 4;      // b=5: 32 x 32 x 4
+constexpr int kLutF = kLut5 + 32 * 32 * 4;      // b=6,7,8: plain fp16 tables at +0, +128, +384
+constexpr int kQimg = kLutF + 1024;             // [slot][set][hi,lo][lane] x 8 B
+constexpr int kQimgBytes = kMaxSlots * 2 * 2 * 64 * 8;
+constexpr int kGmeta = kQimg + kQimgBytes;      // [group] packed metadata
+constexpr int kLdsBytes = kGmeta + 64;
+static_assert(kLdsBytes <= 80 * 1024, "two workgroups per CU");
+
+__device__ __forceinline__ uint32_t lds32(const uint8_t* s, uint32_t off) {
+  return *reinterpret_cast<const uint32_t*>(s + off);
+}
+__device__ __forceinline__ uint2 lds64(const uint8_t* s, uint32_t off) {
+  return *reinterpret_cast<const uint2*>(s + off);
+}
+__device__ __forceinline__ uint32_t lds16(const uint8_t* s, uint32_t off) {
+  return *reinterpret_cast<const uint16_t*>(s + off);
+}
+__device__ __forceinline__ half4_t as_half4(uint32_t lo, uint32_t hi) {
+  return __builtin_bit_cast(half4_t, make_uint2(lo, hi));
+}
+__device__ __forceinline__ float h2f(uint32_t bits16) {
+  return __half2float(__ushort_as_half(static_cast<unsigned short>(bits16)));
+}
+
+// Bits [POS, POS + LEN) of the little-endian word array w (LEN <= 32).
+template <int POS, int LEN, int N>
+__device__ __forceinline__ uint32_t field(const uint32_t (&w)[N]) {
+  constexpr int wi = POS / 32, sh = POS % 32;
+  static_assert(wi < N, "field word");
+  uint32_t v;
+  if constexpr (sh == 0) {
+    v = w[wi];
+  } else if constexpr (sh + LEN <= 32) {
+    v = w[wi] >> sh;
+  } else {
+    static_assert(wi + 1 < N, "field word");
+    v = __builtin_amdgcn_alignbit(w[wi + 1], w[wi], sh);
+  }
+  if constexpr (LEN < 32) v &= (1u << LEN) - 1u;
+  return v;
+}
+
+// Lane-replicated lookup-table base of width b (entry stride 128 B for the
+// replicated tables, 2 B for the plain b >= 6 ones).
+__device__ __forceinline__ uint32_t lut_base(int b, int lane) {
+  const uint32_t rep16 = (lane & 15) * 8, rep32 = (lane & 31) * 4;
+  switch (b) {
+    case 1: return kLut1 + rep16;
+    case 2: return kLut2 + rep16;
+    case 3: return kLut3 + rep32;
+    case 4: return kLut4 + rep32;
+    case 5: return kLut5 + rep32;
+    case 6: return kLutF;
+    case 7: return kLutF + 128;
+    default: return kLutF + 384;
+  }
+}
+
+// Four consecutive B-bit codes starting at stream bit POS of w -> four fp16
+// centroids (MFMA operand).  lb is the lane's table base for width B.
+template <int B, int POS, int N>
+__device__ __forceinline__ half4_t decode4(const uint8_t* smem, const uint32_t (&w)[N], uint32_t lb) {
+  if constexpr (B <= 2) {
+    const uint2 u = lds64(smem, lb + (field<POS, 4 * B>(w) << 7));
+    return as_half4(u.x, u.y);
+  } else if constexpr (B == 3) {
+    return as_half4(lds32(smem, lb + (field<POS, 6>(w) << 7)), lds32(smem, lb + (field<POS + 6, 6>(w) << 7)));
+  } else {
+    constexpr int LS = B <= 5 ? 7 : 1;
+    const uint32_t c0 = lds16(smem, lb + (field<POS, B>(w) << LS));
+    const uint32_t c1 = lds16(smem, lb + (field<POS + B, B>(w) << LS));
+    const uint32_t c2 = lds16(smem, lb + (field<POS + 2 * B, B>(w) << LS));
+    const uint32_t c3 = lds16(smem, lb + (field<POS + 3 * B, B>(w) << LS));
+    return as_half4(c0 | (c1 << 16), c2 | (c3 << 16));
+  }
+}
+
+// quad_perm DPP move of a 32-bit value (ctrl = p0 | p1<<2 | p2<<4 | p3<<6)
+template <int CTRL>
+__device__ __forceinline__ float qperm(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// 4x4 transpose inside every lane quad: on entry lane p of a quad holds
+// x[r] = M[r][p]; on exit it holds x[t] = M[p][t].
+__device__ __forceinline__ void quad_transpose(float4_t& x, int lane) {
+  const bool odd = lane & 1, hi2 = lane & 2;
+  {
+    const float n0 = qperm<0xB1>(x[0]), n1 = qperm<0xB1>(x[1]);
+    const float n2 = qperm<0xB1>(x[2]), n3 = qperm<0xB1>(x[3]);
+    if (odd) {
+      x[0] = n1;
+      x[2] = n3;
+    } else {
+      x[1] = n0;
+      x[3] = n2;
+    }
+  }
+  {
+    const float n0 = qperm<0x4E>(x[0]), n1 = qperm<0x4E>(x[1]);
+    const float n2 = qperm<0x4E>(x[2]), n3 = qperm<0x4E>(x[3]);
+    if (hi2) {
+      x[0] = n2;
+      x[1] = n3;
+    } else {
+      x[2] = n0;
+      x[3] = n1;
+    }
+  }
+}
+
+__device__ __forceinline__ float xmax16(float v) {  // over lanes with equal (lane & 3)
+  v = fmaxf(v, __shfl_xor(v, 4, 64));
+  v = fmaxf(v, __shfl_xor(v, 8, 64));
+  v = fmaxf(v, __shfl_xor(v, 16, 64));
+  return fmaxf(v, __shfl_xor(v, 32, 64));
+}
+__device__ __forceinline__ float xsum16(float v) {
+  v += __shfl_xor(v, 4, 64);
+  v += __shfl_xor(v, 8, 64);
+  v += __shfl_xor(v, 16, 64);
+  return v + __shfl_xor(v, 32, 64);
+}
+
+// ---------------------------------------------------------------- QK chunk
+// One 16-step query slot of a group with code width B, processed in
+// sub-chunks of SUB steps whose 4 B SUB bits are first realigned to bit 0 of a
+// small word array, so every step's field has a constant position.
+template <int B>
+constexpr int qk_sub() { return B <= 2 ? 16 : (B <= 4 ? 8 : 4); }
+template <int B>
+constexpr int qk_words() { return (qk_sub<B>() * 4 * B + 31) / 32; }
+
+template <int B, int NSET, int BASE, int KK>
+__device__ __forceinline__ void qk_step(const uint8_t* smem, const uint32_t (&aw)[qk_words<B>() + 1], int m,
+                                        uint32_t lb, const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
+                                        float4_t (&ah)[NSET], float4_t (&al)[NSET]) {
+  if (BASE + KK < m) {
+    const half4_t kv = decode4<B, 4 * B * KK>(smem, aw, lb);
+#pragma unroll
+    for (int s = 0; s < NSET; ++s) {
+      ah[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(qh[s], kv, ah[s], 4, BASE + KK, 0);
+      al[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(ql[s], kv, al[s], 4, BASE + KK, 0);
+    }
+  }
+}
+
+template <int B, int NSET, int BASE, int... KK>
+__device__ __forceinline__ void qk_steps(std::integer_sequence<int, KK...>, const uint8_t* smem,
+                                         const uint32_t (&aw)[qk_words<B>() + 1], int m, uint32_t lb,
+                                         const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
+                                         float4_t (&ah)[NSET], float4_t (&al)[NSET]) {
+  (qk_step<B, NSET, BASE, KK>(smem, aw, m, lb, qh, ql, ah, al), ...);
+}
+
+template <int B, int NSET, int KWB, int SC>
+__device__ __forceinline__ void qk_sub_chunk(const uint8_t* smem, const uint32_t (&rw)[KWB + 1], int oc, int m,
+                                             uint32_t lb, const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
+                                             float4_t (&ah)[NSET], float4_t (&al)[NSET]) {
+  constexpr int SUB = qk_sub<B>(), NW = qk_words<B>();
+  if (SC * SUB < m) {
+    const int o = oc + SC * SUB * 4 * B;
+    const int w0 = o >> 5, sh = o & 31;
+    uint32_t aw[NW + 1];
+    uint32_t prev = rw[w0];
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const uint32_t nx = rw[min(w0 + i + 1, KWB)];
+      aw[i] = __builtin_amdgcn_alignbit(nx, prev, sh);
+      prev = nx;
+    }
+    aw[NW] = 0;
+    qk_steps<B, NSET, SC * SUB>(std::make_integer_sequence<int, SUB>{}, smem, aw, m, lb, qh, ql, ah, al);
+  }
+}
+
+template <int B, int NSET, int KWB, int... SC>
+__device__ __forceinline__ void qk_sub_chunks(std::integer_sequence<int, SC...>, const uint8_t* smem,
+                                              const uint32_t (&rw)[KWB + 1], int oc, int m, uint32_t lb,
+                                              const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
+                                              float4_t (&ah)[NSET], float4_t (&al)[NSET]) {
+  (qk_sub_chunk<B, NSET, KWB, SC>(smem, rw, oc, m, lb, qh, ql, ah, al), ...);
+}
+
+// m (<= 16) steps of one slot starting at stream bit oc of the row rw.
+template <int B, int NSET, int KWB>
+__device__ __forceinline__ void qk_chunk(const uint8_t* smem, const uint32_t (&rw)[KWB + 1], int oc, int m,
+                                         uint32_t lb, const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
+                                         float4_t (&ah)[NSET], float4_t (&al)[NSET]) {
+  qk_sub_chunks<B, NSET, KWB>(std::make_integer_sequence<int, 16 / qk_sub<B>()>{}, smem, rw, oc, m, lb, qh, ql, ah,
+                              al);
+}
+
+// ---------------------------------------------------------------- PV tile
+template <int BV, int NSET, int S>
+__device__ __forceinline__ void pv_step(const uint8_t* smem, const uint32_t (&vw)[4][BV + 1], uint32_t lb,
+                                        const half4_t (&pp)[NSET], float4_t (&O)[NSET][2]) {
+  constexpr int tau = S >> 3, sp = S & 7;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const half4_t vv = decode4<BV, 4 * BV * sp>(smem, vw[tau * 2 + h], lb);
+#pragma unroll
+    for (int s = 0; s < NSET; ++s) O[s][h] = __builtin_amdgcn_mfma_f32_4x4x4f16(pp[s], vv, O[s][h], 4, S, 0);
+  }
+}
+
+template <int BV, int NSET, int... S>
+__device__ __forceinline__ void pv_steps(std::integer_sequence<int, S...>, const uint8_t* smem,
+                                         const uint32_t (&vw)[4][BV + 1], uint32_t lb, const half4_t (&pp)[NSET],
+                                         float4_t (&O)[NSET][2]) {
+  (pv_step<BV, NSET, S>(smem, vw, lb, pp, O), ...);
+}
+
+// Key data of one 64-token tile (loaded one tile ahead of its use): rw =
+// the key row of token t0 + lane, kn = that token's group radii.
+template <int KWB>
+__device__ __forceinline__ void load_keys(uint32_t (&rw)[KWB + 1], uint32_t (&kn)[kMaxGroups], const CachePtrs& c,
+                                          size_t row, int cap, int kw, int ng, int t0, int lane) {
+  const int tk = t0 + lane;
+#pragma unroll
+  for (int i = 0; i <= KWB; ++i) rw[i] = 0;
+  if (tk < cap) {
+    const uint32_t* src = c.k_codes + (row * cap + tk) * kw;
+    if ((kw & 3) == 0) {
+#pragma unroll
+      for (int i = 0; i < KWB; i += 4) {
+        if (i < kw) {
+          const uint4 v = *reinterpret_cast<const uint4*>(src + i);
+          rw[i] = v.x;
+          rw[i + 1] = v.y;
+          rw[i + 2] = v.z;
+          rw[i + 3] = v.w;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < KWB; ++i)
+        if (i < kw) rw[i] = src[i];
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < kMaxGroups; ++g)
+    kn[g] = (g < ng && tk < cap) ? c.k_norms[(row * kMaxGroups + g) * cap + tk] : 0u;
+}
+
+// Value data of one 64-token tile (loaded when the tile starts, used after
+// its QK products): vn = the value radii of tokens t0 + 4(lane/4) .. +3, vw =
+// the value words of dims lane and 64 + lane of both value tiles.
+template <int BV>
+__device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][BV + 1], const CachePtrs& c, size_t row,
+                                            int cap, int t0, int lane) {
+  const int tq = t0 + 4 * (lane >> 2);
+  vn = tq < cap ? *reinterpret_cast<const uint2*>(c.v_norms + row * cap + tq) : make_uint2(0, 0);
+  const int T0 = t0 / kTile, tiles_left = cap / kTile - T0;
+  const uint32_t* vbase = c.v_codes + (row * (cap / kTile) + T0) * kHeadDim * BV;
+#pragma unroll
+  for (int th = 0; th < 4; ++th) {
+    const int tau = th >> 1, h = th & 1;
+#pragma unroll
+    for (int w = 0; w <= BV; ++w) vw[th][w] = 0;
+    if (tau < tiles_left) {
+      const uint32_t* src = vbase + (static_cast<size_t>(tau) * kHeadDim + 64 * h + lane) * BV;
+      if constexpr (BV % 4 == 0) {
+#pragma unroll
+        for (int w = 0; w < BV; w += 4) {
+          const uint4 v4 = *reinterpret_cast<const uint4*>(src + w);
+          vw[th][w] = v4.x;
+          vw[th][w + 1] = v4.y;
+          vw[th][w + 2] = v4.z;
+          vw[th][w + 3] = v4.w;
+        }
+      } else if constexpr (BV % 2 == 0) {
+#pragma unroll
+        for (int w = 0; w < BV; w += 2) {
+          const uint2 v2 = *reinterpret_cast<const uint2*>(src + w);
+          vw[th][w] = v2.x;
+          vw[th][w + 1] = v2.y;
+        }
+      } else {
+#pragma unroll
+        for (int w = 0; w < BV; ++w) vw[th][w] = src[w];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- kernel
+template <int NSET, int KWB, int BV>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_split_mfma(Dims d, const uint8_t* __restrict__ blob,
+                                                         const int32_t* __restrict__ ctx_len, CachePtrs c,
+                                                         const float* __restrict__ qp, float* __restrict__ part,
+                                                         int n_splits, int split_len) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int bq = lane >> 2, jq = lane & 3;
+  const int split = blockIdx.x, kvh = blockIdx.y, lz = blockIdx.z;
+  const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
+  const int seq = lz % d.batch;
+  const int G = d.group, hqn = d.n_kv * G;
+  const int cap = d.capacity, kw = d.k_words;
+  const RowMeta* M = reinterpret_cast<const RowMeta*>(blob + kOffRows) + (layer * d.n_kv + kvh);
+  const uint16_t* c16 = reinterpret_cast<const uint16_t*>(blob + kOffC16);
+  const int ng = M->n_groups;
+
+  // ---- lookup tables
+  for (int i = tid; i < 16 * 16; i += kThreads) {
+    const int e = i >> 4;
+    const uint16_t* cb = c16 + cb_index(1);
+    *reinterpret_cast<uint2*>(smem + kLut1 + i * 8) =
+        make_uint2(cb[e & 1] | (static_cast<uint32_t>(cb[(e >> 1) & 1]) << 16),
+                   cb[(e >> 2) & 1] | (static_cast<uint32_t>(cb[(e >> 3) & 1]) << 16));
+  }
+  for (int i = tid; i < 256 * 16; i += kThreads) {
+    const int e = i >> 4;
+    const uint16_t* cb = c16 + cb_index(2);
+    *reinterpret_cast<uint2*>(smem + kLut2 + i * 8) =
+        make_uint2(cb[e & 3] | (static_cast<uint32_t>(cb[(e >> 2) & 3]) << 16),
+                   cb[(e >> 4) & 3] | (static_cast<uint32_t>(cb[(e >> 6) & 3]) << 16));
+  }
+  for (int i = tid; i < 64 * 32; i += kThreads) {
+    const int e = i >> 5;
+    const uint16_t* cb = c16 + cb_index(3);
+    *reinterpret_cast<uint32_t*>(smem + kLut3 + i * 4) = cb[e & 7] | (static_cast<uint32_t>(cb[(e >> 3) & 7]) << 16);
+  }
+  for (int i = tid; i < 16 * 32; i += kThreads)
+    *reinterpret_cast<uint32_t*>(smem + kLut4 + i * 4) = c16[cb_index(4) + (i >> 5)];
+  for (int i = tid; i < 32 * 32; i += kThreads)
+    *reinterpret_cast<uint32_t*>(smem + kLut5 + i * 4) = c16[cb_index(5) + (i >> 5)];
+  for (int i = tid; i < 64 + 128 + 256; i += kThreads) {
+    const int b = i < 64 ? 6 : (i < 192 ? 7 : 8);
+    const int k = i < 64 ? i : (i < 192 ? i - 64 : i - 192);
+    *reinterpret_cast<uint16_t*>(smem + kLutF + i * 2) = c16[cb_index(b) + k];
+  }
+  // ---- group metadata: bits 0..9 stream bit offset, 10..13 width, 14..19
+  // steps, 20..23 first query slot.  Each group's steps start a new slot.
+  if (tid == 0) {
+    uint32_t slot = 0;
+    for (int g = 0; g < ng; ++g) {
+      const uint32_t nst = (M->g_dim[g] + 3) / 4;
+      reinterpret_cast<uint32_t*>(smem + kGmeta)[g] = static_cast<uint32_t>(M->bitoff[M->g_pos[g]]) |
+                                                     (static_cast<uint32_t>(M->g_bits[g]) << 10) | (nst << 14) |
+                                                     (slot << 20);
+      slot += (nst + 15) / 16;
+    }
+  }
+  __syncthreads();
+  // ---- query image: slot (g, c), lane 4b+i holds step 16c+b of group g,
+  // head i of each set, 4 coordinates, as fp16 hi and lo parts
+  {
+    const float* qbase = qp + (static_cast<size_t>(lz) * hqn + kvh * G) * kHeadDim;
+    for (int g = 0; g < ng; ++g) {
+      const uint32_t meta = lds32(smem, kGmeta + 4 * g);
+      const int nst = (meta >> 14) & 63, slot0 = (meta >> 20) & 15;
+      const int gpos = M->g_pos[g], gdim = M->g_dim[g];
+      const int nchunk = (nst + 15) / 16;
+      for (int i = tid; i < nchunk * NSET * 64 * 4; i += kThreads) {
+        const int k = i & 3, l = (i >> 2) & 63, set = (i >> 8) % NSET, ch = (i >> 8) / NSET;
+        const int step = 16 * ch + (l >> 2), q = 4 * set + (l & 3), coord = 4 * step + k;
+        float v = 0.f;
+        if (step < nst && coord < gdim && q < G) v = qbase[q * kHeadDim + gpos + coord];
+        const _Float16 hi = static_cast<_Float16>(v);
+        const _Float16 lo = static_cast<_Float16>(v - static_cast<float>(hi));
+        uint8_t* dst = smem + kQimg + ((((slot0 + ch) * 2 + set) * 2) * 64 + l) * 8 + k * 2;
+        *reinterpret_cast<_Float16*>(dst) = hi;
+        *reinterpret_cast<_Float16*>(dst + 64 * 8) = lo;
+      }
+    }
+  }
+  __syncthreads();
+
+  const int ctx = min(ctx_len[seq], cap);
+  const int t_begin = split * split_len;
+  const int t_end = min(t_begin + split_len, ctx);
+  const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + kvh;
+  const float vscale = 0.08838834764831845f;  // 1/sqrt(128)
+
+  float m_run[NSET], l_run[NSET];
+  float4_t O[NSET][2];
+#pragma unroll
+  for (int s = 0; s < NSET; ++s) {
+    m_run[s] = kNegInf;
+    l_run[s] = 0.f;
+    O[s][0] = float4_t{0.f, 0.f, 0.f, 0.f};
+    O[s][1] = float4_t{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // Each wave walks its 64-token tiles with the next tile's loads in flight
+  // while the current one is computed.
+  const int stride = kWaves * 64;
+  int t0 = t_begin + wave * 64;
+  uint32_t rw[KWB + 1], kn[kMaxGroups], rw2[KWB + 1], kn2[kMaxGroups], vw[4][BV + 1];
+  uint2 vn;
+  if (t0 < t_end) load_keys<KWB>(rw, kn, c, row, cap, kw, ng, t0, lane);
+  for (; t0 < t_end; t0 += stride) {
+    load_values<BV>(vn, vw, c, row, cap, t0, lane);
+    if (t0 + stride < t_end) load_keys<KWB>(rw2, kn2, c, row, cap, kw, ng, t0 + stride, lane);
+    const int tk = t0 + lane;
+
+    // ---------------- QK, one same-rate group at a time (lane = token)
+    float4_t L[NSET];
+#pragma unroll
+    for (int s = 0; s < NSET; ++s) L[s] = float4_t{0.f, 0.f, 0.f, 0.f};
+    for (int g = 0; g < ng; ++g) {
+      const uint32_t meta = __builtin_amdgcn_readfirstlane(lds32(smem, kGmeta + 4 * g));
+      const int o = meta & 1023, b = (meta >> 10) & 15, nst = (meta >> 14) & 63, slot0 = (meta >> 20) & 15;
+      const float nrm = h2f(kn[g]);
+      const uint32_t lb = lut_base(b, lane);
+      float4_t ah[NSET], al[NSET];
+#pragma unroll
+      for (int s = 0; s < NSET; ++s) {
+        ah[s] = float4_t{0.f, 0.f, 0.f, 0.f};
+        al[s] = float4_t{0.f, 0.f, 0.f, 0.f};
+      }
+      for (int ch = 0; ch * 16 < nst; ++ch) {
+        half4_t qh[NSET], ql[NSET];
+#pragma unroll
+        for (int s = 0; s < NSET; ++s) {
+          const uint32_t base = kQimg + (((slot0 + ch) * 2 + s) * 2 * 64 + lane) * 8;
+          const uint2 uh = lds64(smem, base), ul = lds64(smem, base + 64 * 8);
+          qh[s] = as_half4(uh.x, uh.y);
+          ql[s] = as_half4(ul.x, ul.y);
+        }
+        const int oc = o + 64 * b * ch, m = min(16, nst - 16 * ch);
+        switch (b) {
+          case 1: qk_chunk<1, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
+          case 2: qk_chunk<2, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
+          case 3: qk_chunk<3, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
+          case 4: qk_chunk<4, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
+          case 5: qk_chunk<5, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
+          case 6: qk_chunk<6, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
+          case 7: qk_chunk<7, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
+          default: qk_chunk<8, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
+        }
+      }
+#pragma unroll
+      for (int s = 0; s < NSET; ++s)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) L[s][r] = fmaf(nrm, ah[s][r] + al[s][r], L[s][r]);
+    }
+
+    // ---------------- online softmax (lane 4b+i: head i, tokens 4b..4b+3)
+    const bool tok_in = tk < t_end;
+    const float vn4[4] = {h2f(vn.x & 0xFFFFu) * vscale, h2f(vn.x >> 16) * vscale,
+                          h2f(vn.y & 0xFFFFu) * vscale, h2f(vn.y >> 16) * vscale};
+    half4_t pp[NSET];
+#pragma unroll
+    for (int s = 0; s < NSET; ++s) {
+      float4_t x = L[s];
+      if (!tok_in) x = float4_t{kNegInf, kNegInf, kNegInf, kNegInf};
+      quad_transpose(x, lane);
+      float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+      mx = xmax16(mx);
+      const float mn = fmaxf(m_run[s], mx);
+      const float corr = m_run[s] == kNegInf ? 0.f : __expf(m_run[s] - mn);
+      float ps = 0.f;
+      uint32_t ph[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = __expf(x[r] - mn);
+        ps += p;
+        const float pv = (t0 + 4 * bq + r < t_end) ? p * vn4[r] : 0.f;
+        ph[r] = __half_as_ushort(__float2half_rn(pv));
+      }
+      pp[s] = as_half4(ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16));
+      ps = xsum16(ps);
+      l_run[s] = l_run[s] * corr + ps;
+      m_run[s] = mn;
+      const float c0 = qperm<0x00>(corr), c1 = qperm<0x55>(corr), c2 = qperm<0xAA>(corr), c3 = qperm<0xFF>(corr);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        O[s][h][0] *= c0;
+        O[s][h][1] *= c1;
+        O[s][h][2] *= c2;
+        O[s][h][3] *= c3;
+      }
+    }
+
+    // ---------------- PV: 16 steps of 4 tokens (lane = dim)
+    pv_steps<BV, NSET>(std::make_integer_sequence<int, 16>{}, smem, vw, lut_base(BV, lane), pp, O);
+#pragma unroll
+    for (int i = 0; i <= KWB; ++i) rw[i] = rw2[i];
+#pragma unroll
+    for (int g = 0; g < kMaxGroups; ++g) kn[g] = kn2[g];
+  }
+
+  // ---------------- merge the 8 waves of the workgroup
+  __syncthreads();
+  float* fm = reinterpret_cast<float*>(smem);            // [wave][8] max
+  float* fl = fm + kWaves * 8;                           // [wave][8] sum
+  float* fo = fl + kWaves * 8;                           // [wave][8][128] accumulators
+#pragma unroll
+  for (int s = 0; s < NSET; ++s) {
+    if (bq == 0) {
+      fm[wave * 8 + s * 4 + jq] = m_run[s];
+      fl[wave * 8 + s * 4 + jq] = l_run[s];
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) fo[(wave * 8 + s * 4 + r) * kHeadDim + 64 * h + lane] = O[s][h][r];
+  }
+  __syncthreads();
+  for (int i = tid; i < G * kHeadDim; i += kThreads) {
+    const int q = i >> 7, dd = i & 127;
+    float mx = kNegInf;
+    for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, fm[w * 8 + q]);
+    float l = 0.f, a = 0.f;
+    if (mx != kNegInf) {
+      for (int w = 0; w < kWaves; ++w) {
+        const float mw = fm[w * 8 + q];
+        if (mw == kNegInf) continue;
+        const float e = __expf(mw - mx);
+        l = fmaf(fl[w * 8 + q], e, l);
+        a = fmaf(fo[(w * 8 + q) * kHeadDim + dd], e, a);
+      }
+    }
+    float* pb = part + ((static_cast<size_t>(lz) * hqn + kvh * G + q) * n_splits + split) * 130;
+    pb[2 + dd] = a;
+    if (dd == 0) {
+      pb[0] = mx;
+      pb[1] = l;
+    }
+  }
+}
+
+// Launch the split pass for value width BV (one instantiation per file).
+template <int BV>
+hipError_t launch_split_bv_impl(const Dims& d, const void* layout, const int32_t* ctx_len, const CachePtrs& c,
+                           const DecodeWs& ws, hipStream_t s) {
+  dim3 grid(ws.n_splits, d.n_kv, d.batch * d.n_lc);
+  const uint8_t* blob = static_cast<const uint8_t*>(layout);
+  const auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, d, blob, ctx_len, c, ws.qp, ws.part, ws.n_splits,
+                       ws.split_len);
+  };
+  if (d.group <= 4) {
+    if (d.k_words <= 8) go(k_split_mfma<1, 8, BV>);
+    else if (d.k_words <= 16) go(k_split_mfma<1, 16, BV>);
+    else go(k_split_mfma<1, 32, BV>);
+  } else {
+    if (d.k_words <= 8) go(k_split_mfma<2, 8, BV>);
+    else if (d.k_words <= 16) go(k_split_mfma<2, 16, BV>);
+    else go(k_split_mfma<2, 32, BV>);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace split_detail
+}  // namespace bgtq

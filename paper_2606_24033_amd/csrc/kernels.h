@@ -31,9 +31,20 @@ struct DecodeWs {
   int split_len;    // tokens per split, multiple of 32
 };
 
-// Split pass of the packed decode (decode.hip); writes ws.part.
-hipError_t launch_split_mfma(const Dims& d, const void* layout, const int32_t* ctx_len, const CachePtrs& c,
-                             const DecodeWs& ws, hipStream_t s);
+// Split pass of the packed decode (decode_impl.h), one entry per value code
+// width (decode_bv1.hip .. decode_bv8.hip); each writes ws.part.
+#define BGTQ_DECL_SPLIT(N)                                                                              \
+  hipError_t launch_split_bv##N(const Dims& d, const void* layout, const int32_t* ctx_len, const CachePtrs& c, \
+                                const DecodeWs& ws, hipStream_t s);
+BGTQ_DECL_SPLIT(1)
+BGTQ_DECL_SPLIT(2)
+BGTQ_DECL_SPLIT(3)
+BGTQ_DECL_SPLIT(4)
+BGTQ_DECL_SPLIT(5)
+BGTQ_DECL_SPLIT(6)
+BGTQ_DECL_SPLIT(7)
+BGTQ_DECL_SPLIT(8)
+#undef BGTQ_DECL_SPLIT
 
 hipError_t launch_decode_packed(const Dims& d, const void* layout, const void* q,
                                 const int32_t* ctx_len, const CachePtrs& c, float* out,

@@ -3,7 +3,7 @@
 //  k_quantize      : TQ-MSE encode (Sec. 2.2) of appended K rows per same-rate
 //                    group (end of Sec. 3.2) and of V rows, dense b-bit pack.
 //  k_qrot          : Q-side rotation of the decode queries (Sec. 4).
-//  (the split pass over the packed cache lives in decode.hip)
+//  (the split pass over the packed cache lives in decode_impl.h)
 //  k_merge         : exact log-sum-exp merge of the splits + inverse V rotation.
 //  k_split_fp16    : the same decode over an fp16 cache (comparator).
 #include <hip/hip_fp16.h>
@@ -367,7 +367,17 @@ hipError_t launch_decode_packed(const Dims& d, const void* layout, const void* q
   const uint8_t* blob = static_cast<const uint8_t*>(layout);
   const int hqn = d.n_kv * d.group;
   hipLaunchKernelGGL(k_qrot, dim3(hqn, d.batch, d.n_lc), dim3(128), 0, s, d, blob, q, ws.qp);
-  hipError_t e = launch_split_mfma(d, layout, ctx_len, c, ws, s);
+  hipError_t e;
+  switch (d.v_bits) {
+    case 1: e = launch_split_bv1(d, layout, ctx_len, c, ws, s); break;
+    case 2: e = launch_split_bv2(d, layout, ctx_len, c, ws, s); break;
+    case 3: e = launch_split_bv3(d, layout, ctx_len, c, ws, s); break;
+    case 4: e = launch_split_bv4(d, layout, ctx_len, c, ws, s); break;
+    case 5: e = launch_split_bv5(d, layout, ctx_len, c, ws, s); break;
+    case 6: e = launch_split_bv6(d, layout, ctx_len, c, ws, s); break;
+    case 7: e = launch_split_bv7(d, layout, ctx_len, c, ws, s); break;
+    default: e = launch_split_bv8(d, layout, ctx_len, c, ws, s); break;
+  }
   if (e != hipSuccess) return e;
   const float* rotv = reinterpret_cast<const float*>(blob + kOffRotV);
   hipLaunchKernelGGL(k_merge, dim3(hqn, d.batch, d.n_lc), dim3(128), 0, s, d, ws.part, ws.n_splits,
