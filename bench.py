@@ -207,10 +207,10 @@ def main():
     dec_gbs = step_bytes / (dec_med * 1e-6) / 1e9
 
     result = {
-        "metric": "packed-KV decode attention us/step + effective HBM GB/s (% of peak) at 128K ctx",
+        "metric": "packed-KV decode attention \u00b5s/step + effective HBM GB/s (% of peak) at 128K ctx",
         "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32", "data": "synthetic",
+        "dtype": "f16", "data": "synthetic",
         "config": {"workload": "Llama-3.1-8B-shaped full decode step: 32 layers x 8 KV heads (32 q heads), "
                                f"d_h 128, {T} cached rows, K2V2, batch 1, bf16 inputs",
                    "global_batch": 1, "seq_len": T, "parallelism": "none (1 GPU)", "n_splits": args.n_splits},

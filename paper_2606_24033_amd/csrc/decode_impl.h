@@ -9,7 +9,7 @@
 // shared by all 64 lanes is held once per 16 steps instead of once per step:
 //  * QK  D_b = A x B_b.  A = 4 rotated-query heads x 4 coordinates of one
 //    decode step, taken from block ABID = step % 16 of a register image in
-//    which lane 4b+i holds step b of a 16-step chunk for head i.
+//    which lane 4b+i holds step b of a 16-step slot for head i.
 //    B_b column j = the 4 dequantized coordinates of token 4b+j: lane l
 //    decodes the key row of token l, 4 stream positions per step.  All lanes
 //    decode the same positions in a step, so they share one code width and a
@@ -21,9 +21,18 @@
 //    contiguous there).  D lands as lane = dim, register = head.
 // Between the two, a 4x4 transpose inside each lane quad turns (token, head)
 // into (head, 4 tokens), the layout of the PV A operand and of the softmax.
+//
+// Same-rate groups have distinct widths, so the QK loop is unrolled over the
+// width b = 1..8 (absent widths skipped by a uniform branch): the width, the
+// lookup table and the register that holds the group radius are compile-time
+// constants.  A group's steps are processed in sub-chunks of 8 (b <= 4) or 4
+// steps whose bits are first realigned to bit 0 of a small word array; inside
+// a sub-chunk all table lookups are issued before the first MFMA that needs
+// them (two passes entered at the step count, so no step is padded).
+//
 // Dequantization goes through lookup tables in LDS, replicated per lane so
-// random indices never collide on a bank: 4 codes per lookup for b <= 2 (a
-// 64-bit entry of four fp16 centroids), 2 codes for b = 3, 1 code above.
+// random indices rarely collide on a bank: 4 codes per lookup for b <= 2 (a
+// 64-bit entry of four fp16 centroids), 2 codes for b = 3, 4, 1 code above.
 // The rotated query is split into fp16 hi and lo parts (both multiplied,
 // accumulated in fp32): fp16 alone leaves ~2^-12 relative error per term.
 #pragma once
@@ -43,21 +52,29 @@ typedef float float4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
-constexpr int kMaxSlots = 10;  // 16-step query chunks of one key row: sum_g ceil(steps_g / 16)
+constexpr int kMaxSlots = 10;  // 16-step query slots of one key row: sum_g ceil(steps_g / 16)
 constexpr float kNegInf = -__builtin_huge_valf();
 
-// LDS map (bytes)
-constexpr int kLut1 = 0;                        // b=1: 16 entries x 16 replicas x 8 B
-constexpr int kLut2 = kLut1 + 16 * 16 * 8;      // b=2: 256 x 16 x 8
+// LDS map (bytes).  Entry strides: 128 B for the 16- and 32-replica tables,
+// 32 B for the 8-replica b = 4 table, 2 B for the plain b >= 6 tables.
+constexpr int kLut1 = 0;                        // b=1: 16 entries (4 codes) x 16 replicas x 8 B
+constexpr int kLut2 = kLut1 + 16 * 16 * 8;      // b=2: 256 (4 codes) x 16 x 8
 constexpr int kLut3 = kLut2 + 256 * 16 * 8;     // b=3: 64 (2 codes) x 32 x 4
-constexpr int kLut4 = kLut3 + 64 * 32 * 4;      // b=4: 16 x 32 x 4 (fp16 in the low half)
-constexpr int kLut5 = kLut4 + 16 * 32 * 4;      // b=5: 32 x 32 x 4
+constexpr int kLut4 = kLut3 + 64 * 32 * 4;      // b=4: 256 (2 codes) x 8 x 4
+constexpr int kLut5 = kLut4 + 256 * 8 * 4;      // b=5: 32 (1 code, low half) x 32 x 4
 constexpr int kLutF = kLut5 + 32 * 32 * 4;      // b=6,7,8: plain fp16 tables at +0, +128, +384
 constexpr int kQimg = kLutF + 1024;             // [slot][set][hi,lo][lane] x 8 B
 constexpr int kQimgBytes = kMaxSlots * 2 * 2 * 64 * 8;
-constexpr int kGmeta = kQimg + kQimgBytes;      // [group] packed metadata
+constexpr int kGmeta = kQimg + kQimgBytes;      // [b - 1] packed group metadata
 constexpr int kLdsBytes = kGmeta + 64;
 static_assert(kLdsBytes <= 80 * 1024, "two workgroups per CU");
+
+// Packed group metadata, indexed by width: bit 31 present, bits 0..9 first
+// stream bit, 10..15 steps, 16..19 first query slot, 20..22 radius plane.
+__device__ __forceinline__ int gm_off(uint32_t gm) { return gm & 1023; }
+__device__ __forceinline__ int gm_steps(uint32_t gm) { return (gm >> 10) & 63; }
+__device__ __forceinline__ int gm_slot(uint32_t gm) { return (gm >> 16) & 15; }
+__device__ __forceinline__ int gm_plane(uint32_t gm) { return (gm >> 20) & 7; }
 
 __device__ __forceinline__ uint32_t lds32(const uint8_t* s, uint32_t off) {
   return *reinterpret_cast<const uint32_t*>(s + off);
@@ -73,59 +90,6 @@ __device__ __forceinline__ half4_t as_half4(uint32_t lo, uint32_t hi) {
 }
 __device__ __forceinline__ float h2f(uint32_t bits16) {
   return __half2float(__ushort_as_half(static_cast<unsigned short>(bits16)));
-}
-
-// Bits [POS, POS + LEN) of the little-endian word array w (LEN <= 32).
-template <int POS, int LEN, int N>
-__device__ __forceinline__ uint32_t field(const uint32_t (&w)[N]) {
-  constexpr int wi = POS / 32, sh = POS % 32;
-  static_assert(wi < N, "field word");
-  uint32_t v;
-  if constexpr (sh == 0) {
-    v = w[wi];
-  } else if constexpr (sh + LEN <= 32) {
-    v = w[wi] >> sh;
-  } else {
-    static_assert(wi + 1 < N, "field word");
-    v = __builtin_amdgcn_alignbit(w[wi + 1], w[wi], sh);
-  }
-  if constexpr (LEN < 32) v &= (1u << LEN) - 1u;
-  return v;
-}
-
-// Lane-replicated lookup-table base of width b (entry stride 128 B for the
-// replicated tables, 2 B for the plain b >= 6 ones).
-__device__ __forceinline__ uint32_t lut_base(int b, int lane) {
-  const uint32_t rep16 = (lane & 15) * 8, rep32 = (lane & 31) * 4;
-  switch (b) {
-    case 1: return kLut1 + rep16;
-    case 2: return kLut2 + rep16;
-    case 3: return kLut3 + rep32;
-    case 4: return kLut4 + rep32;
-    case 5: return kLut5 + rep32;
-    case 6: return kLutF;
-    case 7: return kLutF + 128;
-    default: return kLutF + 384;
-  }
-}
-
-// Four consecutive B-bit codes starting at stream bit POS of w -> four fp16
-// centroids (MFMA operand).  lb is the lane's table base for width B.
-template <int B, int POS, int N>
-__device__ __forceinline__ half4_t decode4(const uint8_t* smem, const uint32_t (&w)[N], uint32_t lb) {
-  if constexpr (B <= 2) {
-    const uint2 u = lds64(smem, lb + (field<POS, 4 * B>(w) << 7));
-    return as_half4(u.x, u.y);
-  } else if constexpr (B == 3) {
-    return as_half4(lds32(smem, lb + (field<POS, 6>(w) << 7)), lds32(smem, lb + (field<POS + 6, 6>(w) << 7)));
-  } else {
-    constexpr int LS = B <= 5 ? 7 : 1;
-    const uint32_t c0 = lds16(smem, lb + (field<POS, B>(w) << LS));
-    const uint32_t c1 = lds16(smem, lb + (field<POS + B, B>(w) << LS));
-    const uint32_t c2 = lds16(smem, lb + (field<POS + 2 * B, B>(w) << LS));
-    const uint32_t c3 = lds16(smem, lb + (field<POS + 3 * B, B>(w) << LS));
-    return as_half4(c0 | (c1 << 16), c2 | (c3 << 16));
-  }
 }
 
 // quad_perm DPP move of a 32-bit value (ctrl = p0 | p1<<2 | p2<<4 | p3<<6)
@@ -175,44 +139,123 @@ __device__ __forceinline__ float xsum16(float v) {
   return v + __shfl_xor(v, 32, 64);
 }
 
-// ---------------------------------------------------------------- QK chunk
-// One 16-step query slot of a group with code width B, processed in
-// sub-chunks of SUB steps whose 4 B SUB bits are first realigned to bit 0 of a
-// small word array, so every step's field has a constant position.
-template <int B>
-constexpr int qk_sub() { return B <= 2 ? 16 : (B <= 4 ? 8 : 4); }
-template <int B>
-constexpr int qk_words() { return (qk_sub<B>() * 4 * B + 31) / 32; }
+// Bits [POS, POS + LEN) of the little-endian word array w (LEN <= 32).
+template <int POS, int LEN, int N>
+__device__ __forceinline__ uint32_t field(const uint32_t (&w)[N]) {
+  constexpr int wi = POS / 32, sh = POS % 32;
+  static_assert(wi < N, "field word");
+  uint32_t v;
+  if constexpr (sh == 0) {
+    v = w[wi];
+  } else if constexpr (sh + LEN <= 32) {
+    v = w[wi] >> sh;
+  } else {
+    static_assert(wi + 1 < N, "field word");
+    v = __builtin_amdgcn_alignbit(w[wi + 1], w[wi], sh);
+  }
+  if constexpr (LEN < 32) v &= (1u << LEN) - 1u;
+  return v;
+}
 
-template <int B, int NSET, int BASE, int KK>
-__device__ __forceinline__ void qk_step(const uint8_t* smem, const uint32_t (&aw)[qk_words<B>() + 1], int m,
-                                        uint32_t lb, const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
-                                        float4_t (&ah)[NSET], float4_t (&al)[NSET]) {
-  if (BASE + KK < m) {
-    const half4_t kv = decode4<B, 4 * B * KK>(smem, aw, lb);
-#pragma unroll
-    for (int s = 0; s < NSET; ++s) {
-      ah[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(qh[s], kv, ah[s], 4, BASE + KK, 0);
-      al[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(ql[s], kv, al[s], 4, BASE + KK, 0);
-    }
+// Per-lane replica offsets of the lookup tables.
+struct LaneRep {
+  uint32_t r16;  // (lane & 15) * 8
+  uint32_t r32;  // (lane & 31) * 4
+  uint32_t r8;   // (lane & 7) * 4
+};
+
+// Four consecutive B-bit codes starting at bit POS of w -> four fp16
+// centroids (an MFMA operand).
+template <int B, int POS, int N>
+__device__ __forceinline__ half4_t decode4(const uint8_t* smem, const uint32_t (&w)[N], const LaneRep& r) {
+  if constexpr (B <= 2) {
+    constexpr int base = B == 1 ? kLut1 : kLut2;
+    const uint2 u = lds64(smem, base + r.r16 + (field<POS, 4 * B>(w) << 7));
+    return as_half4(u.x, u.y);
+  } else if constexpr (B == 3) {
+    return as_half4(lds32(smem, kLut3 + r.r32 + (field<POS, 6>(w) << 7)),
+                    lds32(smem, kLut3 + r.r32 + (field<POS + 6, 6>(w) << 7)));
+  } else if constexpr (B == 4) {
+    return as_half4(lds32(smem, kLut4 + r.r8 + (field<POS, 8>(w) << 5)),
+                    lds32(smem, kLut4 + r.r8 + (field<POS + 8, 8>(w) << 5)));
+  } else {
+    constexpr int LS = B == 5 ? 7 : 1;
+    constexpr int base = B == 5 ? kLut5 : (B == 6 ? kLutF : (B == 7 ? kLutF + 128 : kLutF + 384));
+    const uint32_t rb = B == 5 ? r.r32 : 0u;
+    const uint32_t c0 = lds16(smem, base + rb + (field<POS, B>(w) << LS));
+    const uint32_t c1 = lds16(smem, base + rb + (field<POS + B, B>(w) << LS));
+    const uint32_t c2 = lds16(smem, base + rb + (field<POS + 2 * B, B>(w) << LS));
+    const uint32_t c3 = lds16(smem, base + rb + (field<POS + 3 * B, B>(w) << LS));
+    return as_half4(c0 | (c1 << 16), c2 | (c3 << 16));
   }
 }
 
-template <int B, int NSET, int BASE, int... KK>
-__device__ __forceinline__ void qk_steps(std::integer_sequence<int, KK...>, const uint8_t* smem,
-                                         const uint32_t (&aw)[qk_words<B>() + 1], int m, uint32_t lb,
-                                         const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
-                                         float4_t (&ah)[NSET], float4_t (&al)[NSET]) {
-  (qk_step<B, NSET, BASE, KK>(smem, aw, m, lb, qh, ql, ah, al), ...);
-}
+// ---------------------------------------------------------------- QK
+template <int B>
+constexpr int qk_ch() { return B <= 4 ? 8 : 4; }           // steps per sub-chunk
+template <int B>
+constexpr int qk_nw() { return (qk_ch<B>() * 4 * B + 31) / 32; }  // words per sub-chunk
 
+// mm (1..CH) steps of a sub-chunk whose first step uses query block K0.
+#define BGTQ_DEC(k) kv[k] = decode4<B, 4 * B * (k)>(smem, aw, rep)
+#define BGTQ_MAC(k)                                                                       \
+  _Pragma("unroll") for (int s = 0; s < NSET; ++s) {                                     \
+    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(qh[s], kv[k], acc[s], 4, K0 + (k), 0);   \
+    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(ql[s], kv[k], acc[s], 4, K0 + (k), 0);   \
+  }
+template <int B, int NSET, int K0>
+__device__ __forceinline__ void qk_sub(const uint8_t* smem, const uint32_t (&aw)[qk_nw<B>() + 1], int mm,
+                                       const LaneRep& rep, const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
+                                       float4_t (&acc)[NSET]) {
+  half4_t kv[qk_ch<B>()];
+  if constexpr (qk_ch<B>() == 8) {
+    switch (mm) {
+      default: BGTQ_DEC(7); [[fallthrough]];
+      case 7: BGTQ_DEC(6); [[fallthrough]];
+      case 6: BGTQ_DEC(5); [[fallthrough]];
+      case 5: BGTQ_DEC(4); [[fallthrough]];
+      case 4: BGTQ_DEC(3); [[fallthrough]];
+      case 3: BGTQ_DEC(2); [[fallthrough]];
+      case 2: BGTQ_DEC(1); [[fallthrough]];
+      case 1: BGTQ_DEC(0);
+    }
+    switch (mm) {
+      default: BGTQ_MAC(7) [[fallthrough]];
+      case 7: BGTQ_MAC(6) [[fallthrough]];
+      case 6: BGTQ_MAC(5) [[fallthrough]];
+      case 5: BGTQ_MAC(4) [[fallthrough]];
+      case 4: BGTQ_MAC(3) [[fallthrough]];
+      case 3: BGTQ_MAC(2) [[fallthrough]];
+      case 2: BGTQ_MAC(1) [[fallthrough]];
+      case 1: BGTQ_MAC(0)
+    }
+  } else {
+    switch (mm) {
+      default: BGTQ_DEC(3); [[fallthrough]];
+      case 3: BGTQ_DEC(2); [[fallthrough]];
+      case 2: BGTQ_DEC(1); [[fallthrough]];
+      case 1: BGTQ_DEC(0);
+    }
+    switch (mm) {
+      default: BGTQ_MAC(3) [[fallthrough]];
+      case 3: BGTQ_MAC(2) [[fallthrough]];
+      case 2: BGTQ_MAC(1) [[fallthrough]];
+      case 1: BGTQ_MAC(0)
+    }
+  }
+}
+#undef BGTQ_DEC
+#undef BGTQ_MAC
+
+// Sub-chunk SC of a 16-step slot: realign its bits (stream bit ob onwards)
+// to bit 0 of aw, then run its min(CH, ms - SC CH) steps.
 template <int B, int NSET, int KWB, int SC>
-__device__ __forceinline__ void qk_sub_chunk(const uint8_t* smem, const uint32_t (&rw)[KWB + 1], int oc, int m,
-                                             uint32_t lb, const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
-                                             float4_t (&ah)[NSET], float4_t (&al)[NSET]) {
-  constexpr int SUB = qk_sub<B>(), NW = qk_words<B>();
-  if (SC * SUB < m) {
-    const int o = oc + SC * SUB * 4 * B;
+__device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t (&rw)[KWB + 1], int ob, int ms,
+                                             const LaneRep& rep, const half4_t (&qh)[NSET],
+                                             const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
+  constexpr int CH = qk_ch<B>(), NW = qk_nw<B>();
+  if (SC * CH < ms) {
+    const int o = ob + SC * CH * 4 * B;
     const int w0 = o >> 5, sh = o & 31;
     uint32_t aw[NW + 1];
     uint32_t prev = rw[w0];
@@ -223,35 +266,56 @@ __device__ __forceinline__ void qk_sub_chunk(const uint8_t* smem, const uint32_t
       prev = nx;
     }
     aw[NW] = 0;
-    qk_steps<B, NSET, SC * SUB>(std::make_integer_sequence<int, SUB>{}, smem, aw, m, lb, qh, ql, ah, al);
+    qk_sub<B, NSET, SC * CH>(smem, aw, min(CH, ms - SC * CH), rep, qh, ql, acc);
   }
 }
 
 template <int B, int NSET, int KWB, int... SC>
-__device__ __forceinline__ void qk_sub_chunks(std::integer_sequence<int, SC...>, const uint8_t* smem,
-                                              const uint32_t (&rw)[KWB + 1], int oc, int m, uint32_t lb,
-                                              const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
-                                              float4_t (&ah)[NSET], float4_t (&al)[NSET]) {
-  (qk_sub_chunk<B, NSET, KWB, SC>(smem, rw, oc, m, lb, qh, ql, ah, al), ...);
+__device__ __forceinline__ void qk_slot(std::integer_sequence<int, SC...>, const uint8_t* smem,
+                                        const uint32_t (&rw)[KWB + 1], int ob, int ms, const LaneRep& rep,
+                                        const half4_t (&qh)[NSET], const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
+  (qk_slot_part<B, NSET, KWB, SC>(smem, rw, ob, ms, rep, qh, ql, acc), ...);
 }
 
-// m (<= 16) steps of one slot starting at stream bit oc of the row rw.
+// The group of width B (metadata gm, radius bits nrm16 of the lane's token):
+// L += radius * <rotated query, dequantized unit-norm codes>.
 template <int B, int NSET, int KWB>
-__device__ __forceinline__ void qk_chunk(const uint8_t* smem, const uint32_t (&rw)[KWB + 1], int oc, int m,
-                                         uint32_t lb, const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
-                                         float4_t (&ah)[NSET], float4_t (&al)[NSET]) {
-  qk_sub_chunks<B, NSET, KWB>(std::make_integer_sequence<int, 16 / qk_sub<B>()>{}, smem, rw, oc, m, lb, qh, ql, ah,
-                              al);
+__device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&rw)[KWB + 1], uint32_t gm,
+                                         uint32_t nrm16, const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
+  const int o = gm_off(gm), nst = gm_steps(gm), slot0 = gm_slot(gm);
+  float4_t acc[NSET];
+#pragma unroll
+  for (int s = 0; s < NSET; ++s) acc[s] = float4_t{0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c * 16 < nst; ++c) {
+    half4_t qh[NSET], ql[NSET];
+#pragma unroll
+    for (int s = 0; s < NSET; ++s) {
+      const uint32_t base = kQimg + (((slot0 + c) * 2 + s) * 2 * 64 + lane) * 8;
+      const uint2 uh = lds64(smem, base), ul = lds64(smem, base + 64 * 8);
+      qh[s] = as_half4(uh.x, uh.y);
+      ql[s] = as_half4(ul.x, ul.y);
+    }
+    qk_slot<B, NSET, KWB>(std::make_integer_sequence<int, 16 / qk_ch<B>()>{}, smem, rw, o + 64 * B * c,
+                          min(16, nst - 16 * c), rep, qh, ql, acc);
+  }
+  const float nrm = h2f(nrm16);
+#pragma unroll
+  for (int s = 0; s < NSET; ++s)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) L[s][r] = fmaf(nrm, acc[s][r], L[s][r]);
 }
 
-// ---------------------------------------------------------------- PV tile
+// ---------------------------------------------------------------- PV
+template <int BV>
+constexpr int pv_words() { return BV; }
+
 template <int BV, int NSET, int S>
-__device__ __forceinline__ void pv_step(const uint8_t* smem, const uint32_t (&vw)[4][BV + 1], uint32_t lb,
-                                        const half4_t (&pp)[NSET], float4_t (&O)[NSET][2]) {
+__device__ __forceinline__ void pv_step(const uint8_t* smem, const uint32_t (&vw)[4][pv_words<BV>()],
+                                        const LaneRep& rep, const half4_t (&pp)[NSET], float4_t (&O)[NSET][2]) {
   constexpr int tau = S >> 3, sp = S & 7;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const half4_t vv = decode4<BV, 4 * BV * sp>(smem, vw[tau * 2 + h], lb);
+    const half4_t vv = decode4<BV, 4 * BV * sp>(smem, vw[tau * 2 + h], rep);
 #pragma unroll
     for (int s = 0; s < NSET; ++s) O[s][h] = __builtin_amdgcn_mfma_f32_4x4x4f16(pp[s], vv, O[s][h], 4, S, 0);
   }
@@ -259,20 +323,23 @@ __device__ __forceinline__ void pv_step(const uint8_t* smem, const uint32_t (&vw
 
 template <int BV, int NSET, int... S>
 __device__ __forceinline__ void pv_steps(std::integer_sequence<int, S...>, const uint8_t* smem,
-                                         const uint32_t (&vw)[4][BV + 1], uint32_t lb, const half4_t (&pp)[NSET],
-                                         float4_t (&O)[NSET][2]) {
-  (pv_step<BV, NSET, S>(smem, vw, lb, pp, O), ...);
+                                         const uint32_t (&vw)[4][pv_words<BV>()], const LaneRep& rep,
+                                         const half4_t (&pp)[NSET], float4_t (&O)[NSET][2]) {
+  (pv_step<BV, NSET, S>(smem, vw, rep, pp, O), ...);
 }
 
-// Key data of one 64-token tile (loaded one tile ahead of its use): rw =
-// the key row of token t0 + lane, kn = that token's group radii.
+// ---------------------------------------------------------------- loads
+// Key data of one 64-token tile (loaded one tile ahead of its use): rw = the
+// key row of token t0 + lane, knp[(b - 1) / 2] half (b - 1) & 1 = that
+// token's radius of the width-b group.
 template <int KWB>
-__device__ __forceinline__ void load_keys(uint32_t (&rw)[KWB + 1], uint32_t (&kn)[kMaxGroups], const CachePtrs& c,
-                                          size_t row, int cap, int kw, int ng, int t0, int lane) {
+__device__ __forceinline__ void load_keys(uint32_t (&rw)[KWB + 1], uint32_t (&knp)[4], const uint32_t (&gmb)[8],
+                                          const CachePtrs& c, size_t row, int cap, int kw, int t0, int lane) {
   const int tk = t0 + lane;
+  const bool ok = tk < cap;
 #pragma unroll
   for (int i = 0; i <= KWB; ++i) rw[i] = 0;
-  if (tk < cap) {
+  if (ok) {
     const uint32_t* src = c.k_codes + (row * cap + tk) * kw;
     if ((kw & 3) == 0) {
 #pragma unroll
@@ -291,17 +358,23 @@ __device__ __forceinline__ void load_keys(uint32_t (&rw)[KWB + 1], uint32_t (&kn
         if (i < kw) rw[i] = src[i];
     }
   }
+  const uint16_t* nb = c.k_norms + row * kMaxGroups * cap + tk;
 #pragma unroll
-  for (int g = 0; g < kMaxGroups; ++g)
-    kn[g] = (g < ng && tk < cap) ? c.k_norms[(row * kMaxGroups + g) * cap + tk] : 0u;
+  for (int p = 0; p < 4; ++p) {
+    uint32_t lo = 0, hi = 0;
+    if ((gmb[2 * p] >> 31) && ok) lo = nb[static_cast<size_t>(gm_plane(gmb[2 * p])) * cap];
+    if ((gmb[2 * p + 1] >> 31) && ok) hi = nb[static_cast<size_t>(gm_plane(gmb[2 * p + 1])) * cap];
+    knp[p] = lo | (hi << 16);
+  }
 }
 
 // Value data of one 64-token tile (loaded when the tile starts, used after
 // its QK products): vn = the value radii of tokens t0 + 4(lane/4) .. +3, vw =
 // the value words of dims lane and 64 + lane of both value tiles.
 template <int BV>
-__device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][BV + 1], const CachePtrs& c, size_t row,
-                                            int cap, int t0, int lane) {
+__device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][pv_words<BV>()], const CachePtrs& c,
+                                            size_t row, int cap, int t0, int lane) {
+  constexpr int NW = pv_words<BV>();
   const int tq = t0 + 4 * (lane >> 2);
   vn = tq < cap ? *reinterpret_cast<const uint2*>(c.v_norms + row * cap + tq) : make_uint2(0, 0);
   const int T0 = t0 / kTile, tiles_left = cap / kTile - T0;
@@ -310,7 +383,7 @@ __device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][BV + 1]
   for (int th = 0; th < 4; ++th) {
     const int tau = th >> 1, h = th & 1;
 #pragma unroll
-    for (int w = 0; w <= BV; ++w) vw[th][w] = 0;
+    for (int w = 0; w < NW; ++w) vw[th][w] = 0;
     if (tau < tiles_left) {
       const uint32_t* src = vbase + (static_cast<size_t>(tau) * kHeadDim + 64 * h + lane) * BV;
       if constexpr (BV % 4 == 0) {
@@ -337,12 +410,22 @@ __device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][BV + 1]
   }
 }
 
+// QK of one tile over every present width.
+template <int NSET, int KWB, int... BM1>
+__device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const uint8_t* smem,
+                                       const uint32_t (&rw)[KWB + 1], const uint32_t (&knp)[4],
+                                       const uint32_t (&gmb)[8], const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
+  ((gmb[BM1] >> 31 ? qk_group<BM1 + 1, NSET, KWB>(smem, rw, gmb[BM1], (knp[BM1 / 2] >> (16 * (BM1 & 1))) & 0xFFFFu,
+                                                  rep, lane, L)
+                   : void()),
+   ...);
+}
+
 // ---------------------------------------------------------------- kernel
 template <int NSET, int KWB, int BV>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_split_mfma(Dims d, const uint8_t* __restrict__ blob,
-                                                         const int32_t* __restrict__ ctx_len, CachePtrs c,
-                                                         const float* __restrict__ qp, float* __restrict__ part,
-                                                         int n_splits, int split_len) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 16 ? 3 : 4))) void k_split_mfma(
+    Dims d, const uint8_t* __restrict__ blob, const int32_t* __restrict__ ctx_len, CachePtrs c,
+    const float* __restrict__ qp, float* __restrict__ part, int n_splits, int split_len) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bq = lane >> 2, jq = lane & 3;
@@ -375,8 +458,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     const uint16_t* cb = c16 + cb_index(3);
     *reinterpret_cast<uint32_t*>(smem + kLut3 + i * 4) = cb[e & 7] | (static_cast<uint32_t>(cb[(e >> 3) & 7]) << 16);
   }
-  for (int i = tid; i < 16 * 32; i += kThreads)
-    *reinterpret_cast<uint32_t*>(smem + kLut4 + i * 4) = c16[cb_index(4) + (i >> 5)];
+  for (int i = tid; i < 256 * 8; i += kThreads) {
+    const int e = i >> 3;
+    const uint16_t* cb = c16 + cb_index(4);
+    *reinterpret_cast<uint32_t*>(smem + kLut4 + i * 4) = cb[e & 15] | (static_cast<uint32_t>(cb[e >> 4]) << 16);
+  }
   for (int i = tid; i < 32 * 32; i += kThreads)
     *reinterpret_cast<uint32_t*>(smem + kLut5 + i * 4) = c16[cb_index(5) + (i >> 5)];
   for (int i = tid; i < 64 + 128 + 256; i += kThreads) {
@@ -384,26 +470,27 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     const int k = i < 64 ? i : (i < 192 ? i - 64 : i - 192);
     *reinterpret_cast<uint16_t*>(smem + kLutF + i * 2) = c16[cb_index(b) + k];
   }
-  // ---- group metadata: bits 0..9 stream bit offset, 10..13 width, 14..19
-  // steps, 20..23 first query slot.  Each group's steps start a new slot.
+  // ---- group metadata by width; each group's steps start a new query slot
+  if (tid < 8) reinterpret_cast<uint32_t*>(smem + kGmeta)[tid] = 0u;
+  __syncthreads();
   if (tid == 0) {
     uint32_t slot = 0;
     for (int g = 0; g < ng; ++g) {
       const uint32_t nst = (M->g_dim[g] + 3) / 4;
-      reinterpret_cast<uint32_t*>(smem + kGmeta)[g] = static_cast<uint32_t>(M->bitoff[M->g_pos[g]]) |
-                                                     (static_cast<uint32_t>(M->g_bits[g]) << 10) | (nst << 14) |
-                                                     (slot << 20);
+      reinterpret_cast<uint32_t*>(smem + kGmeta)[M->g_bits[g] - 1] =
+          (1u << 31) | static_cast<uint32_t>(M->bitoff[M->g_pos[g]]) | (nst << 10) | (slot << 16) |
+          (static_cast<uint32_t>(g) << 20);
       slot += (nst + 15) / 16;
     }
   }
   __syncthreads();
-  // ---- query image: slot (g, c), lane 4b+i holds step 16c+b of group g,
-  // head i of each set, 4 coordinates, as fp16 hi and lo parts
+  // ---- query image: slot s, lane 4b+i holds step 16(s - slot0_g) + b of
+  // group g, head i of each set, 4 coordinates, as fp16 hi and lo parts
   {
     const float* qbase = qp + (static_cast<size_t>(lz) * hqn + kvh * G) * kHeadDim;
     for (int g = 0; g < ng; ++g) {
-      const uint32_t meta = lds32(smem, kGmeta + 4 * g);
-      const int nst = (meta >> 14) & 63, slot0 = (meta >> 20) & 15;
+      const uint32_t meta = lds32(smem, kGmeta + 4 * (M->g_bits[g] - 1));
+      const int nst = gm_steps(meta), slot0 = gm_slot(meta);
       const int gpos = M->g_pos[g], gdim = M->g_dim[g];
       const int nchunk = (nst + 15) / 16;
       for (int i = tid; i < nchunk * NSET * 64 * 4; i += kThreads) {
@@ -421,6 +508,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   }
   __syncthreads();
 
+  uint32_t gmb[8];
+#pragma unroll
+  for (int b = 0; b < 8; ++b) gmb[b] = __builtin_amdgcn_readfirstlane(lds32(smem, kGmeta + 4 * b));
+  const LaneRep rep{static_cast<uint32_t>(lane & 15) * 8u, static_cast<uint32_t>(lane & 31) * 4u,
+                    static_cast<uint32_t>(lane & 7) * 4u};
+
   const int ctx = min(ctx_len[seq], cap);
   const int t_begin = split * split_len;
   const int t_end = min(t_begin + split_len, ctx);
@@ -437,59 +530,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     O[s][1] = float4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  // Each wave walks its 64-token tiles with the next tile's loads in flight
+  // Each wave walks its 64-token tiles with the next tile's keys in flight
   // while the current one is computed.
   const int stride = kWaves * 64;
   int t0 = t_begin + wave * 64;
-  uint32_t rw[KWB + 1], kn[kMaxGroups], rw2[KWB + 1], kn2[kMaxGroups], vw[4][BV + 1];
+  uint32_t rw[KWB + 1], knp[4], rw2[KWB + 1], knp2[4], vw[4][pv_words<BV>()];
   uint2 vn;
-  if (t0 < t_end) load_keys<KWB>(rw, kn, c, row, cap, kw, ng, t0, lane);
+  if (t0 < t_end) load_keys<KWB>(rw, knp, gmb, c, row, cap, kw, t0, lane);
   for (; t0 < t_end; t0 += stride) {
     load_values<BV>(vn, vw, c, row, cap, t0, lane);
-    if (t0 + stride < t_end) load_keys<KWB>(rw2, kn2, c, row, cap, kw, ng, t0 + stride, lane);
+    if (t0 + stride < t_end) load_keys<KWB>(rw2, knp2, gmb, c, row, cap, kw, t0 + stride, lane);
     const int tk = t0 + lane;
 
     // ---------------- QK, one same-rate group at a time (lane = token)
     float4_t L[NSET];
 #pragma unroll
     for (int s = 0; s < NSET; ++s) L[s] = float4_t{0.f, 0.f, 0.f, 0.f};
-    for (int g = 0; g < ng; ++g) {
-      const uint32_t meta = __builtin_amdgcn_readfirstlane(lds32(smem, kGmeta + 4 * g));
-      const int o = meta & 1023, b = (meta >> 10) & 15, nst = (meta >> 14) & 63, slot0 = (meta >> 20) & 15;
-      const float nrm = h2f(kn[g]);
-      const uint32_t lb = lut_base(b, lane);
-      float4_t ah[NSET], al[NSET];
-#pragma unroll
-      for (int s = 0; s < NSET; ++s) {
-        ah[s] = float4_t{0.f, 0.f, 0.f, 0.f};
-        al[s] = float4_t{0.f, 0.f, 0.f, 0.f};
-      }
-      for (int ch = 0; ch * 16 < nst; ++ch) {
-        half4_t qh[NSET], ql[NSET];
-#pragma unroll
-        for (int s = 0; s < NSET; ++s) {
-          const uint32_t base = kQimg + (((slot0 + ch) * 2 + s) * 2 * 64 + lane) * 8;
-          const uint2 uh = lds64(smem, base), ul = lds64(smem, base + 64 * 8);
-          qh[s] = as_half4(uh.x, uh.y);
-          ql[s] = as_half4(ul.x, ul.y);
-        }
-        const int oc = o + 64 * b * ch, m = min(16, nst - 16 * ch);
-        switch (b) {
-          case 1: qk_chunk<1, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
-          case 2: qk_chunk<2, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
-          case 3: qk_chunk<3, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
-          case 4: qk_chunk<4, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
-          case 5: qk_chunk<5, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
-          case 6: qk_chunk<6, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
-          case 7: qk_chunk<7, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
-          default: qk_chunk<8, NSET, KWB>(smem, rw, oc, m, lb, qh, ql, ah, al); break;
-        }
-      }
-#pragma unroll
-      for (int s = 0; s < NSET; ++s)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) L[s][r] = fmaf(nrm, ah[s][r] + al[s][r], L[s][r]);
-    }
+    qk_all<NSET, KWB>(std::make_integer_sequence<int, 8>{}, smem, rw, knp, gmb, rep, lane, L);
 
     // ---------------- online softmax (lane 4b+i: head i, tokens 4b..4b+3)
     const bool tok_in = tk < t_end;
@@ -529,11 +586,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     }
 
     // ---------------- PV: 16 steps of 4 tokens (lane = dim)
-    pv_steps<BV, NSET>(std::make_integer_sequence<int, 16>{}, smem, vw, lut_base(BV, lane), pp, O);
+    pv_steps<BV, NSET>(std::make_integer_sequence<int, 16>{}, smem, vw, rep, pp, O);
 #pragma unroll
     for (int i = 0; i <= KWB; ++i) rw[i] = rw2[i];
 #pragma unroll
-    for (int g = 0; g < kMaxGroups; ++g) kn[g] = kn2[g];
+    for (int p = 0; p < 4; ++p) knp[p] = knp2[p];
   }
 
   // ---------------- merge the 8 waves of the workgroup
@@ -579,7 +636,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
 // Launch the split pass for value width BV (one instantiation per file).
 template <int BV>
 hipError_t launch_split_bv_impl(const Dims& d, const void* layout, const int32_t* ctx_len, const CachePtrs& c,
-                           const DecodeWs& ws, hipStream_t s) {
+                                const DecodeWs& ws, hipStream_t s) {
   dim3 grid(ws.n_splits, d.n_kv, d.batch * d.n_lc);
   const uint8_t* blob = static_cast<const uint8_t*>(layout);
   const auto go = [&](auto kern) {
