@@ -126,7 +126,7 @@ def main():
     bg.lib()
     T = args.ctx
     n_extra = args.warmup + args.steps
-    cap = ((T + n_extra + 31) // 32) * 32
+    cap = ((T + n_extra + 63) // 64) * 64
     max_ctx = T + n_extra
     cfg = bg.Config(n_layers=N_LAYERS, batch=1, n_kv_heads=N_KV, group=GROUP, capacity=cap, k_budget=K_BUDGET,
                     v_bits=V_BITS, in_dtype=bg.BGTQ_BF16)

@@ -34,7 +34,7 @@
  *            tile form one 32*b_v-bit string; token slot s = t % 32 occupies
  *            bits [s*b_v, s*b_v + b_v).
  *  v_norms : fp16  [n_layers][batch][n_kv_heads][capacity]
- *  capacity must be a multiple of 32.  The caller zero-fills the cache once.
+ *  capacity must be a multiple of 64.  The caller zero-fills the cache once.
  */
 #ifndef BLOCKGTQ_H
 #define BLOCKGTQ_H
@@ -67,7 +67,7 @@ typedef struct {
   int32_t n_kv_heads;  /* KV heads per layer                                */
   int32_t group;       /* query heads per KV head (G), 1..8                 */
   int32_t head_dim;    /* d_h; must be 128                                  */
-  int32_t capacity;    /* rows per (layer, sequence, KV head); multiple of 32 */
+  int32_t capacity;    /* rows per (layer, sequence, KV head); multiple of 64 */
   int32_t k_budget;    /* B = sum of the 64 block widths of a key head; the
                           K row holds 2B bits (K3 -> 192, K2 -> 128)         */
   int32_t v_bits;      /* b_V, 1..8                                         */

@@ -21,6 +21,10 @@ FLAGS = [
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
     "-Wall", "-Wno-unused-function",
 ]
+# The decode kernels compare softmax scores with max(): no NaN can reach them
+# (finite codebooks and radii, -inf only as a mask), so skip the IEEE
+# canonicalization that would otherwise precede every max.
+DECODE_FLAGS = ["-fno-honor-nans", "-mno-amdgpu-ieee"]
 
 
 def _run(cmd):
@@ -38,7 +42,8 @@ def build(verbose: bool = False) -> str:
     for src in SOURCES:
         obj = os.path.join(BUILD_DIR, src + ".o")
         lang = ["-x", "hip"]
-        cmds.append([HIPCC, *FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj])
+        extra = DECODE_FLAGS if src.startswith("decode_") else []
+        cmds.append([HIPCC, *FLAGS, *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 4, 16)) as ex:
         list(ex.map(_run, cmds))

@@ -177,8 +177,8 @@ int check_cfg(const bgtq_config* c) {
   if (c->n_layers < 1 || c->batch < 1 || c->n_kv_heads < 1)
     return fail(BGTQ_EINVAL, "n_layers, batch and n_kv_heads must be >= 1");
   if (c->group < 1 || c->group > 8) return fail(BGTQ_EUNSUPPORTED, "group %d outside 1..8", c->group);
-  if (c->capacity < kTile || c->capacity % kTile != 0)
-    return fail(BGTQ_EINVAL, "capacity %d must be a positive multiple of 32", c->capacity);
+  if (c->capacity < kKeyTile || c->capacity % kKeyTile != 0)
+    return fail(BGTQ_EINVAL, "capacity %d must be a positive multiple of 64", c->capacity);
   if (c->k_budget < kBlocks || c->k_budget > 8 * kBlocks)
     return fail(BGTQ_EBUDGET, "k_budget %d outside [64, 512]", c->k_budget);
   if (c->v_bits < 1 || c->v_bits > 8) return fail(BGTQ_EINVAL, "v_bits %d outside 1..8", c->v_bits);

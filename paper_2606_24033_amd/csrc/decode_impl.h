@@ -126,17 +126,46 @@ __device__ __forceinline__ void quad_transpose(float4_t& x, int lane) {
   }
 }
 
-__device__ __forceinline__ float xmax16(float v) {  // over lanes with equal (lane & 3)
-  v = fmaxf(v, __shfl_xor(v, 4, 64));
-  v = fmaxf(v, __shfl_xor(v, 8, 64));
-  v = fmaxf(v, __shfl_xor(v, 16, 64));
-  return fmaxf(v, __shfl_xor(v, 32, 64));
+// Rotate right by N lanes inside every 16-lane row (DPP row_ror).
+template <int N>
+__device__ __forceinline__ float row_ror(float v) {
+  return __builtin_bit_cast(float,
+                            __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x120 + N, 0xF, 0xF, false));
+}
+// Lane swaps of gfx950: r0, r1 = the values of rows 2k and 2k+1 (16-lane
+// rows) at this lane's row position, resp. of lanes l % 32 and l % 32 + 32.
+// Written as inline asm with both registers as outputs: the compiler's
+// builtin for these instructions returns the first register twice.  The
+// s_nop pairs cover the VALU-to-permlane operand hazard on either side.
+__device__ __forceinline__ void swap16(float v, float& r0, float& r1) {
+  unsigned x = __builtin_bit_cast(unsigned, v), y = x;
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(x), "+v"(y));
+  r0 = __builtin_bit_cast(float, x);
+  r1 = __builtin_bit_cast(float, y);
+}
+__device__ __forceinline__ void swap32(float v, float& r0, float& r1) {
+  unsigned x = __builtin_bit_cast(unsigned, v), y = x;
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(x), "+v"(y));
+  r0 = __builtin_bit_cast(float, x);
+  r1 = __builtin_bit_cast(float, y);
+}
+// Max / sum over the 16 lanes with equal (lane & 3); every lane gets the
+// same result (the cross-row steps combine rows in a fixed order).
+__device__ __forceinline__ float xmax16(float v) {
+  float a, b;
+  v = fmaxf(v, row_ror<4>(v));
+  v = fmaxf(v, row_ror<8>(v));
+  swap16(v, a, b);
+  swap32(fmaxf(a, b), a, b);
+  return fmaxf(a, b);
 }
 __device__ __forceinline__ float xsum16(float v) {
-  v += __shfl_xor(v, 4, 64);
-  v += __shfl_xor(v, 8, 64);
-  v += __shfl_xor(v, 16, 64);
-  return v + __shfl_xor(v, 32, 64);
+  float a, b;
+  v += row_ror<4>(v);
+  v += row_ror<8>(v);
+  swap16(v, a, b);
+  swap32(a + b, a, b);
+  return a + b;
 }
 
 // Bits [POS, POS + LEN) of the little-endian word array w (LEN <= 32).
@@ -193,64 +222,38 @@ __device__ __forceinline__ half4_t decode4(const uint8_t* smem, const uint32_t (
 // ---------------------------------------------------------------- QK
 template <int B>
 constexpr int qk_ch() { return B <= 4 ? 8 : 4; }           // steps per sub-chunk
+constexpr int kRowPad = 4;  // zero words after a key row: a sub-chunk reads words w0 .. w0 + 4
 template <int B>
 constexpr int qk_nw() { return (qk_ch<B>() * 4 * B + 31) / 32; }  // words per sub-chunk
 
-// mm (1..CH) steps of a sub-chunk whose first step uses query block K0.
-#define BGTQ_DEC(k) kv[k] = decode4<B, 4 * B * (k)>(smem, aw, rep)
-#define BGTQ_MAC(k)                                                                       \
-  _Pragma("unroll") for (int s = 0; s < NSET; ++s) {                                     \
-    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(qh[s], kv[k], acc[s], 4, K0 + (k), 0);   \
-    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(ql[s], kv[k], acc[s], 4, K0 + (k), 0);   \
-  }
-template <int B, int NSET, int K0>
-__device__ __forceinline__ void qk_sub(const uint8_t* smem, const uint32_t (&aw)[qk_nw<B>() + 1], int mm,
-                                       const LaneRep& rep, const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
-                                       float4_t (&acc)[NSET]) {
-  half4_t kv[qk_ch<B>()];
-  if constexpr (qk_ch<B>() == 8) {
-    switch (mm) {
-      default: BGTQ_DEC(7); [[fallthrough]];
-      case 7: BGTQ_DEC(6); [[fallthrough]];
-      case 6: BGTQ_DEC(5); [[fallthrough]];
-      case 5: BGTQ_DEC(4); [[fallthrough]];
-      case 4: BGTQ_DEC(3); [[fallthrough]];
-      case 3: BGTQ_DEC(2); [[fallthrough]];
-      case 2: BGTQ_DEC(1); [[fallthrough]];
-      case 1: BGTQ_DEC(0);
-    }
-    switch (mm) {
-      default: BGTQ_MAC(7) [[fallthrough]];
-      case 7: BGTQ_MAC(6) [[fallthrough]];
-      case 6: BGTQ_MAC(5) [[fallthrough]];
-      case 5: BGTQ_MAC(4) [[fallthrough]];
-      case 4: BGTQ_MAC(3) [[fallthrough]];
-      case 3: BGTQ_MAC(2) [[fallthrough]];
-      case 2: BGTQ_MAC(1) [[fallthrough]];
-      case 1: BGTQ_MAC(0)
-    }
-  } else {
-    switch (mm) {
-      default: BGTQ_DEC(3); [[fallthrough]];
-      case 3: BGTQ_DEC(2); [[fallthrough]];
-      case 2: BGTQ_DEC(1); [[fallthrough]];
-      case 1: BGTQ_DEC(0);
-    }
-    switch (mm) {
-      default: BGTQ_MAC(3) [[fallthrough]];
-      case 3: BGTQ_MAC(2) [[fallthrough]];
-      case 2: BGTQ_MAC(1) [[fallthrough]];
-      case 1: BGTQ_MAC(0)
-    }
+// Steps K..min(mm, KEND)-1 of a sub-chunk, in windows of 4: first every
+// table lookup of the window, then its MFMAs (query block K0 + step), so the
+// lookups overlap each other.
+template <int B, int K, int KEND, int N>
+__device__ __forceinline__ void qk_dec(const uint8_t* smem, const uint32_t (&aw)[N], int mm, const LaneRep& rep,
+                                       half4_t (&kv)[4]) {
+  kv[K & 3] = decode4<B, 4 * B * K>(smem, aw, rep);
+  if constexpr (K + 1 < KEND) {
+    if (mm > K + 1) qk_dec<B, K + 1, KEND, N>(smem, aw, mm, rep, kv);
   }
 }
-#undef BGTQ_DEC
-#undef BGTQ_MAC
+template <int NSET, int K0, int K, int KEND>
+__device__ __forceinline__ void qk_mac(const half4_t (&kv)[4], int mm, const half4_t (&qh)[NSET],
+                                       const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
+#pragma unroll
+  for (int s = 0; s < NSET; ++s) {
+    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(qh[s], kv[K & 3], acc[s], 4, K0 + K, 0);
+    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(ql[s], kv[K & 3], acc[s], 4, K0 + K, 0);
+  }
+  if constexpr (K + 1 < KEND) {
+    if (mm > K + 1) qk_mac<NSET, K0, K + 1, KEND>(kv, mm, qh, ql, acc);
+  }
+}
 
 // Sub-chunk SC of a 16-step slot: realign its bits (stream bit ob onwards)
 // to bit 0 of aw, then run its min(CH, ms - SC CH) steps.
 template <int B, int NSET, int KWB, int SC>
-__device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t (&rw)[KWB + 1], int ob, int ms,
+__device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t (&rw)[KWB + kRowPad], int ob, int ms,
                                              const LaneRep& rep, const half4_t (&qh)[NSET],
                                              const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
   constexpr int CH = qk_ch<B>(), NW = qk_nw<B>();
@@ -258,21 +261,25 @@ __device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t
     const int o = ob + SC * CH * 4 * B;
     const int w0 = o >> 5, sh = o & 31;
     uint32_t aw[NW + 1];
-    uint32_t prev = rw[w0];
 #pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const uint32_t nx = rw[min(w0 + i + 1, KWB)];
-      aw[i] = __builtin_amdgcn_alignbit(nx, prev, sh);
-      prev = nx;
-    }
+    for (int i = 0; i < NW; ++i) aw[i] = __builtin_amdgcn_alignbit(rw[w0 + i + 1], rw[w0 + i], sh);
     aw[NW] = 0;
-    qk_sub<B, NSET, SC * CH>(smem, aw, min(CH, ms - SC * CH), rep, qh, ql, acc);
+    const int mm = min(CH, ms - SC * CH);
+    half4_t kv[4];
+    qk_dec<B, 0, 4, NW + 1>(smem, aw, mm, rep, kv);
+    qk_mac<NSET, SC * CH, 0, 4>(kv, mm, qh, ql, acc);
+    if constexpr (CH == 8) {
+      if (mm > 4) {
+        qk_dec<B, 4, 8, NW + 1>(smem, aw, mm, rep, kv);
+        qk_mac<NSET, SC * CH, 4, 8>(kv, mm, qh, ql, acc);
+      }
+    }
   }
 }
 
 template <int B, int NSET, int KWB, int... SC>
 __device__ __forceinline__ void qk_slot(std::integer_sequence<int, SC...>, const uint8_t* smem,
-                                        const uint32_t (&rw)[KWB + 1], int ob, int ms, const LaneRep& rep,
+                                        const uint32_t (&rw)[KWB + kRowPad], int ob, int ms, const LaneRep& rep,
                                         const half4_t (&qh)[NSET], const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
   (qk_slot_part<B, NSET, KWB, SC>(smem, rw, ob, ms, rep, qh, ql, acc), ...);
 }
@@ -280,7 +287,7 @@ __device__ __forceinline__ void qk_slot(std::integer_sequence<int, SC...>, const
 // The group of width B (metadata gm, radius bits nrm16 of the lane's token):
 // L += radius * <rotated query, dequantized unit-norm codes>.
 template <int B, int NSET, int KWB>
-__device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&rw)[KWB + 1], uint32_t gm,
+__device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&rw)[KWB + kRowPad], uint32_t gm,
                                          uint32_t nrm16, const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
   const int o = gm_off(gm), nst = gm_steps(gm), slot0 = gm_slot(gm);
   float4_t acc[NSET];
@@ -329,83 +336,82 @@ __device__ __forceinline__ void pv_steps(std::integer_sequence<int, S...>, const
 }
 
 // ---------------------------------------------------------------- loads
-// Key data of one 64-token tile (loaded one tile ahead of its use): rw = the
-// key row of token t0 + lane, knp[(b - 1) / 2] half (b - 1) & 1 = that
-// token's radius of the width-b group.
+// Cache rows of one (layer, sequence, KV head).
+struct RowPtrs {
+  const uint32_t* k;   // [cap][kw] key rows
+  const uint16_t* kn;  // [8][cap] group radii
+  const uint32_t* v;   // [cap / 32][128][BV] value tiles
+  const uint16_t* vn;  // [cap] value radii
+};
+
+// Key data of the 64-token tile at t0 (loaded one tile ahead of its use):
+// rw[0..kw) = the key row of token t0 + lane (zero up to KWB), knp[(b - 1) / 2] half
+// (b - 1) & 1 = that token's radius in the width-b group.  Every token of a
+// tile is below the capacity (a multiple of 64).
 template <int KWB>
-__device__ __forceinline__ void load_keys(uint32_t (&rw)[KWB + 1], uint32_t (&knp)[4], const uint32_t (&gmb)[8],
-                                          const CachePtrs& c, size_t row, int cap, int kw, int t0, int lane) {
-  const int tk = t0 + lane;
-  const bool ok = tk < cap;
+__device__ __forceinline__ void load_keys(uint32_t (&rw)[KWB], uint32_t (&knp)[4],
+                                          const uint32_t (&gmb)[8], const RowPtrs& R, int cap, int kw, int t0,
+                                          int lane) {
+  const uint32_t* src = R.k + static_cast<size_t>(t0) * kw;
+  const uint32_t lo = static_cast<uint32_t>(lane * kw);
+  if ((kw & 3) == 0) {
 #pragma unroll
-  for (int i = 0; i <= KWB; ++i) rw[i] = 0;
-  if (ok) {
-    const uint32_t* src = c.k_codes + (row * cap + tk) * kw;
-    if ((kw & 3) == 0) {
-#pragma unroll
-      for (int i = 0; i < KWB; i += 4) {
-        if (i < kw) {
-          const uint4 v = *reinterpret_cast<const uint4*>(src + i);
-          rw[i] = v.x;
-          rw[i + 1] = v.y;
-          rw[i + 2] = v.z;
-          rw[i + 3] = v.w;
-        }
+    for (int i = 0; i < KWB; i += 4) {
+      if (i < kw) {
+        const uint4 v = *reinterpret_cast<const uint4*>(src + lo + i);
+        rw[i] = v.x;
+        rw[i + 1] = v.y;
+        rw[i + 2] = v.z;
+        rw[i + 3] = v.w;
+      } else {
+        rw[i] = rw[i + 1] = rw[i + 2] = rw[i + 3] = 0u;
       }
-    } else {
-#pragma unroll
-      for (int i = 0; i < KWB; ++i)
-        if (i < kw) rw[i] = src[i];
     }
+  } else {
+#pragma unroll
+    for (int i = 0; i < KWB; ++i) rw[i] = i < kw ? src[lo + i] : 0u;
   }
-  const uint16_t* nb = c.k_norms + row * kMaxGroups * cap + tk;
+  const uint16_t* nb = R.kn + t0;
 #pragma unroll
   for (int p = 0; p < 4; ++p) {
-    uint32_t lo = 0, hi = 0;
-    if ((gmb[2 * p] >> 31) && ok) lo = nb[static_cast<size_t>(gm_plane(gmb[2 * p])) * cap];
-    if ((gmb[2 * p + 1] >> 31) && ok) hi = nb[static_cast<size_t>(gm_plane(gmb[2 * p + 1])) * cap];
-    knp[p] = lo | (hi << 16);
+    uint32_t lo16 = 0, hi16 = 0;
+    if (gmb[2 * p] >> 31) lo16 = nb[static_cast<size_t>(gm_plane(gmb[2 * p])) * cap + lane];
+    if (gmb[2 * p + 1] >> 31) hi16 = nb[static_cast<size_t>(gm_plane(gmb[2 * p + 1])) * cap + lane];
+    knp[p] = lo16 | (hi16 << 16);
   }
 }
 
-// Value data of one 64-token tile (loaded when the tile starts, used after
-// its QK products): vn = the value radii of tokens t0 + 4(lane/4) .. +3, vw =
+// Value data of the tile at t0 (loaded when the tile starts, used after its
+// QK products): vn = the value radii of tokens t0 + 4(lane/4) .. +3, vw =
 // the value words of dims lane and 64 + lane of both value tiles.
 template <int BV>
-__device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][pv_words<BV>()], const CachePtrs& c,
-                                            size_t row, int cap, int t0, int lane) {
-  constexpr int NW = pv_words<BV>();
-  const int tq = t0 + 4 * (lane >> 2);
-  vn = tq < cap ? *reinterpret_cast<const uint2*>(c.v_norms + row * cap + tq) : make_uint2(0, 0);
-  const int T0 = t0 / kTile, tiles_left = cap / kTile - T0;
-  const uint32_t* vbase = c.v_codes + (row * (cap / kTile) + T0) * kHeadDim * BV;
+__device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][pv_words<BV>()], const RowPtrs& R, int t0,
+                                            int lane) {
+  vn = *reinterpret_cast<const uint2*>(R.vn + t0 + 4 * (lane >> 2));
+  const uint32_t* vb = R.v + static_cast<size_t>(t0 / kTile) * kHeadDim * BV;
+  const uint32_t lo = static_cast<uint32_t>(lane * BV);
 #pragma unroll
   for (int th = 0; th < 4; ++th) {
-    const int tau = th >> 1, h = th & 1;
+    const uint32_t* src = vb + ((th >> 1) * kHeadDim + 64 * (th & 1)) * BV + lo;
+    if constexpr (BV % 4 == 0) {
 #pragma unroll
-    for (int w = 0; w < NW; ++w) vw[th][w] = 0;
-    if (tau < tiles_left) {
-      const uint32_t* src = vbase + (static_cast<size_t>(tau) * kHeadDim + 64 * h + lane) * BV;
-      if constexpr (BV % 4 == 0) {
-#pragma unroll
-        for (int w = 0; w < BV; w += 4) {
-          const uint4 v4 = *reinterpret_cast<const uint4*>(src + w);
-          vw[th][w] = v4.x;
-          vw[th][w + 1] = v4.y;
-          vw[th][w + 2] = v4.z;
-          vw[th][w + 3] = v4.w;
-        }
-      } else if constexpr (BV % 2 == 0) {
-#pragma unroll
-        for (int w = 0; w < BV; w += 2) {
-          const uint2 v2 = *reinterpret_cast<const uint2*>(src + w);
-          vw[th][w] = v2.x;
-          vw[th][w + 1] = v2.y;
-        }
-      } else {
-#pragma unroll
-        for (int w = 0; w < BV; ++w) vw[th][w] = src[w];
+      for (int w = 0; w < BV; w += 4) {
+        const uint4 v4 = *reinterpret_cast<const uint4*>(src + w);
+        vw[th][w] = v4.x;
+        vw[th][w + 1] = v4.y;
+        vw[th][w + 2] = v4.z;
+        vw[th][w + 3] = v4.w;
       }
+    } else if constexpr (BV % 2 == 0) {
+#pragma unroll
+      for (int w = 0; w < BV; w += 2) {
+        const uint2 v2 = *reinterpret_cast<const uint2*>(src + w);
+        vw[th][w] = v2.x;
+        vw[th][w + 1] = v2.y;
+      }
+    } else {
+#pragma unroll
+      for (int w = 0; w < BV; ++w) vw[th][w] = src[w];
     }
   }
 }
@@ -413,7 +419,7 @@ __device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][pv_word
 // QK of one tile over every present width.
 template <int NSET, int KWB, int... BM1>
 __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const uint8_t* smem,
-                                       const uint32_t (&rw)[KWB + 1], const uint32_t (&knp)[4],
+                                       const uint32_t (&rw)[KWB + kRowPad], const uint32_t (&knp)[4],
                                        const uint32_t (&gmb)[8], const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
   ((gmb[BM1] >> 31 ? qk_group<BM1 + 1, NSET, KWB>(smem, rw, gmb[BM1], (knp[BM1 / 2] >> (16 * (BM1 & 1))) & 0xFFFFu,
                                                   rep, lane, L)
@@ -534,12 +540,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   // while the current one is computed.
   const int stride = kWaves * 64;
   int t0 = t_begin + wave * 64;
-  uint32_t rw[KWB + 1], knp[4], rw2[KWB + 1], knp2[4], vw[4][pv_words<BV>()];
+  const RowPtrs R{c.k_codes + row * cap * kw, c.k_norms + row * kMaxGroups * cap,
+                  c.v_codes + row * (cap / kTile) * kHeadDim * BV, c.v_norms + row * cap};
+  uint32_t rw[KWB + kRowPad], knp[4], rw2[KWB], knp2[4], vw[4][pv_words<BV>()];
   uint2 vn;
-  if (t0 < t_end) load_keys<KWB>(rw, knp, gmb, c, row, cap, kw, t0, lane);
+#pragma unroll
+  for (int i = KWB; i < KWB + kRowPad; ++i) rw[i] = 0u;
+  if (t0 < t_end) load_keys<KWB>(rw2, knp2, gmb, R, cap, kw, t0, lane);
   for (; t0 < t_end; t0 += stride) {
-    load_values<BV>(vn, vw, c, row, cap, t0, lane);
-    if (t0 + stride < t_end) load_keys<KWB>(rw2, knp2, gmb, c, row, cap, kw, t0 + stride, lane);
+#pragma unroll
+    for (int i = 0; i < KWB; ++i) rw[i] = rw2[i];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) knp[p] = knp2[p];
+    load_values<BV>(vn, vw, R, t0, lane);
+    if (t0 + stride < t_end) load_keys<KWB>(rw2, knp2, gmb, R, cap, kw, t0 + stride, lane);
     const int tk = t0 + lane;
 
     // ---------------- QK, one same-rate group at a time (lane = token)
@@ -572,8 +586,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
         ph[r] = __half_as_ushort(__float2half_rn(pv));
       }
       pp[s] = as_half4(ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16));
-      ps = xsum16(ps);
-      l_run[s] = l_run[s] * corr + ps;
+      l_run[s] = l_run[s] * corr + ps;  // this lane's tokens only; reduced after the loop
       m_run[s] = mn;
       const float c0 = qperm<0x00>(corr), c1 = qperm<0x55>(corr), c2 = qperm<0xAA>(corr), c3 = qperm<0xFF>(corr);
 #pragma unroll
@@ -587,11 +600,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
 
     // ---------------- PV: 16 steps of 4 tokens (lane = dim)
     pv_steps<BV, NSET>(std::make_integer_sequence<int, 16>{}, smem, vw, rep, pp, O);
-#pragma unroll
-    for (int i = 0; i <= KWB; ++i) rw[i] = rw2[i];
-#pragma unroll
-    for (int p = 0; p < 4; ++p) knp[p] = knp2[p];
   }
+
+#pragma unroll
+  for (int s = 0; s < NSET; ++s) l_run[s] = xsum16(l_run[s]);
 
   // ---------------- merge the 8 waves of the workgroup
   __syncthreads();

@@ -12,6 +12,7 @@ namespace bgtq {
 constexpr int kHeadDim = 128;        // d_h
 constexpr int kBlocks = 64;          // L = d_h / 2 RoPE blocks
 constexpr int kTile = 32;            // tokens per value tile
+constexpr int kKeyTile = 64;         // tokens per decode tile; the capacity is a multiple of it
 constexpr int kMaxGroups = 8;        // same-rate groups (b = 1..8)
 constexpr int kMaxKWords = 32;       // 128 positions x 8 bits / 32
 constexpr int kMaxSteps = 48;        // 4-coordinate decode steps of a key row (<= 32 + 8)

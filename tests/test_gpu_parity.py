@@ -93,7 +93,7 @@ def test_toy_single_head_end_to_end():
     """1 layer, 1 KV head, G = 4, d_h = 128, base 1e4, 2048 fp32 rows, K3V2,
     allocator on 256 calibration keys; append row 2048, attend 2049 rows."""
     bg = bgm()
-    st = P.make_setup(1, 1, 1, 1, 4, 2080, 192, 2, 1e4, "fp32", n_cal=256)
+    st = P.make_setup(1, 1, 1, 1, 4, 2112, 192, 2, 1e4, "fp32", n_cal=256)
     layout, cache = build(st)
     k, v = P.keys_values(st, 0, 0, 0, 2049)
     append(st, layout, cache, 0, [[(k[:2048], v[:2048])]], [0])
@@ -111,7 +111,7 @@ def test_toy_single_head_end_to_end():
         log("toy n_splits", ns, "rel err", err)
         assert err <= 2e-3
     # fp16 comparator against the definition on fp16-rounded K/V
-    k16 = torch.zeros((1, 1, 1, 2080, 128), dtype=torch.float16, device="cuda")
+    k16 = torch.zeros((1, 1, 1, st.cfg.capacity, 128), dtype=torch.float16, device="cuda")
     v16 = torch.zeros_like(k16)
     k16[0, 0, 0, :2049] = torch.from_numpy(k.astype(np.float32)).half().cuda()
     v16[0, 0, 0, :2049] = torch.from_numpy(v.astype(np.float32)).half().cuda()
