@@ -555,6 +555,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     load_values<BV>(vn, vw, R, t0, lane);
     if (t0 + stride < t_end) load_keys<KWB>(rw2, knp2, gmb, R, cap, kw, t0 + stride, lane);
     const int tk = t0 + lane;
+    {
+      // Re-read the width metadata every tile (through an opaque address):
+      // hoisted out of the loop, its derived scalars exhaust the SGPRs.
+      uint32_t goff = kGmeta;
+      asm volatile("" : "+v"(goff));
+#pragma unroll
+      for (int b = 0; b < 8; ++b) gmb[b] = __builtin_amdgcn_readfirstlane(lds32(smem, goff + 4 * b));
+    }
 
     // ---------------- QK, one same-rate group at a time (lane = token)
     float4_t L[NSET];
