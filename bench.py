@@ -159,7 +159,7 @@ def main():
     wps = torch.arange(T, T + n_extra, dtype=torch.int32, device="cuda")
     ctxs = wps + 1
     out = torch.empty((N_LAYERS, 1, N_KV * GROUP, 128), dtype=torch.float32, device="cuda")
-    ws = torch.empty(bg.workspace_bytes(cfg, N_LAYERS, args.n_splits, max_ctx), dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(bg.workspace_bytes(cfg, N_LAYERS, args.n_splits, max_ctx), dtype=torch.uint8, device="cuda")
     torch.cuda.synchronize()
     log(f"setup {time.time() - t_setup:.1f} s (prefill of {T} rows x {N_LAYERS} layers x {N_KV} heads)")
 

@@ -118,7 +118,11 @@ int blockgtq_cache_bytes(const bgtq_config* cfg, size_t* k_codes, size_t* k_norm
                          size_t* v_codes, size_t* v_norms);
 /* Workspace of one blockgtq_decode_attn call: n_layers_in_call = 1 for a
  * single layer, cfg->n_layers for layer = -1.  n_splits as passed to the
- * call (0 = the heuristic for max_ctx). */
+ * call (0 = the heuristic for max_ctx).  The workspace starts with one int32
+ * counter per (layer in call, sequence, KV head) that the kernel uses to find
+ * the last split to finish: it must be zero-filled once before its first
+ * use, and every completed call leaves it zero again.  Calls that share a
+ * workspace must not overlap in time (one stream, or ordered by events). */
 int blockgtq_workspace_bytes(const bgtq_config* cfg, int32_t n_layers_in_call,
                              int32_t n_splits, int32_t max_ctx, size_t* bytes_out);
 
@@ -169,7 +173,9 @@ int blockgtq_quantize_append(const bgtq_config* cfg, const void* d_layout, int32
  *      gets an all-zero output.
  * max_ctx: host-side upper bound of d_ctx_len (<= capacity), sizes the splits.
  * d_out: float, same shape as d_q.
- * d_workspace / ws_bytes: see blockgtq_workspace_bytes (EWORKSPACE if short).
+ * d_workspace / ws_bytes: see blockgtq_workspace_bytes (EWORKSPACE if short;
+ *      zero-filled before first use).  One kernel launch: the query rotation,
+ *      the split pass and the merge of the splits.
  * n_splits: 0 = heuristic, else 1 .. 4096. */
 int blockgtq_decode_attn(const bgtq_config* cfg, const void* d_layout, int32_t layer,
                          const void* d_q, const int32_t* d_ctx_len, int32_t max_ctx,

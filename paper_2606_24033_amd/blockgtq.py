@@ -238,7 +238,7 @@ def blockgtq_decode_attn(cfg: Config, layout: Layout, layer: int, q, ctx_len, ma
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     if workspace is None:
-        workspace = torch.empty(workspace_bytes(cfg, n_lc, n_splits, max_ctx), dtype=torch.uint8, device=q.device)
+        workspace = torch.zeros(workspace_bytes(cfg, n_lc, n_splits, max_ctx), dtype=torch.uint8, device=q.device)
     _check(lib().blockgtq_decode_attn(ctypes.byref(cfg.c()), _ptr(layout.blob), layer, _ptr(q), _ptr(ctx_len),
                                       max_ctx, ctypes.byref(cache.c()), _ptr(out), _ptr(workspace),
                                       workspace.numel(), n_splits, _stream(stream)))
@@ -256,7 +256,7 @@ def blockgtq_decode_attn_fp16(cfg: Config, layer: int, q, ctx_len, max_ctx: int,
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     if workspace is None:
-        workspace = torch.empty(workspace_bytes(cfg, n_lc, n_splits, max_ctx), dtype=torch.uint8, device=q.device)
+        workspace = torch.zeros(workspace_bytes(cfg, n_lc, n_splits, max_ctx), dtype=torch.uint8, device=q.device)
     _check(lib().blockgtq_decode_attn_fp16(ctypes.byref(cfg.c()), layer, _ptr(q), _ptr(ctx_len), max_ctx,
                                            _ptr(k16), _ptr(v16), _ptr(out), _ptr(workspace), workspace.numel(),
                                            n_splits, _stream(stream)))

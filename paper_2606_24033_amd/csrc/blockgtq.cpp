@@ -227,10 +227,15 @@ SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested
 
 size_t al256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+// Workspace: split counters [n_lc][batch][n_kv] int32, then the split
+// partials [n_lc][batch][Hq][n_splits][130] fp32.
+size_t ws_counter_bytes(const bgtq_config* c, int n_lc) {
+  return al256(static_cast<size_t>(n_lc) * c->batch * c->n_kv_heads * 4);
+}
 size_t ws_bytes_of(const bgtq_config* c, int n_lc, const SplitPlan& p) {
   const size_t hq = static_cast<size_t>(c->n_kv_heads) * c->group;
   const size_t units = static_cast<size_t>(n_lc) * c->batch * hq;
-  return al256(units * kHeadDim * 4) + al256(units * p.n_splits * 130 * 4);
+  return ws_counter_bytes(c, n_lc) + al256(units * p.n_splits * 130 * 4);
 }
 
 }  // namespace
@@ -482,9 +487,8 @@ static int check_decode_args(const bgtq_config* cfg, int32_t layer, const void* 
   const SplitPlan p = plan_splits(cfg, n_lc, max_ctx, n_splits);
   const size_t need = ws_bytes_of(cfg, n_lc, p);
   if (ws_bytes < need) return fail(BGTQ_EWORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
-  const size_t units = static_cast<size_t>(n_lc) * cfg->batch * cfg->n_kv_heads * cfg->group;
-  ws->qp = static_cast<float*>(d_ws);
-  ws->part = reinterpret_cast<float*>(static_cast<uint8_t*>(d_ws) + al256(units * kHeadDim * 4));
+  ws->counters = static_cast<int32_t*>(d_ws);
+  ws->part = reinterpret_cast<float*>(static_cast<uint8_t*>(d_ws) + ws_counter_bytes(cfg, n_lc));
   ws->n_splits = p.n_splits;
   ws->split_len = p.split_len;
   return BGTQ_OK;

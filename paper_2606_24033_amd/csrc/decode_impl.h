@@ -1,6 +1,7 @@
-// Split pass of the packed-cache decode attention for gfx950 (Sec. 4: fused
-// unpack -> codebook -> norm rescale -> QK and PV products -> online softmax,
-// split along the key axis).
+// Packed-cache decode attention for gfx950 in one kernel (Sec. 4: Q-side
+// rotation, then fused unpack -> codebook -> norm rescale -> QK and PV
+// products -> online softmax over a split of the key axis, then the exact
+// log-sum-exp merge of the splits and the inverse V rotation).
 //
 // Work mapping.  One workgroup = 8 waves = one (split, KV head, sequence[,
 // layer]).  A wave owns 64-token tiles (two value tiles).  Both products run
@@ -87,6 +88,10 @@ __device__ __forceinline__ uint32_t lds16(const uint8_t* s, uint32_t off) {
 }
 __device__ __forceinline__ half4_t as_half4(uint32_t lo, uint32_t hi) {
   return __builtin_bit_cast(half4_t, make_uint2(lo, hi));
+}
+__device__ __forceinline__ float ld_q(const void* q, size_t i, int dtype) {  // BGTQ_BF16 = 1
+  if (dtype == 1) return __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(q)[i]) << 16);
+  return reinterpret_cast<const float*>(q)[i];
 }
 __device__ __forceinline__ float h2f(uint32_t bits16) {
   return __half2float(__ushort_as_half(static_cast<unsigned short>(bits16)));
@@ -430,8 +435,9 @@ __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const
 // ---------------------------------------------------------------- kernel
 template <int NSET, int KWB, int BV>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 16 ? 3 : 4))) void k_split_mfma(
-    Dims d, const uint8_t* __restrict__ blob, const int32_t* __restrict__ ctx_len, CachePtrs c,
-    const float* __restrict__ qp, float* __restrict__ part, int n_splits, int split_len) {
+    Dims d, const uint8_t* __restrict__ blob, const void* __restrict__ q, const int32_t* __restrict__ ctx_len,
+    CachePtrs c, float* __restrict__ out, int32_t* __restrict__ counters, float* __restrict__ part, int n_splits,
+    int split_len) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bq = lane >> 2, jq = lane & 3;
@@ -444,6 +450,83 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   const uint16_t* c16 = reinterpret_cast<const uint16_t*>(blob + kOffC16);
   const int ng = M->n_groups;
 
+  // ---- group metadata by width; each group's steps start a new query slot
+  if (tid < 8) reinterpret_cast<uint32_t*>(smem + kGmeta)[tid] = 0u;
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t slot = 0;
+    for (int g = 0; g < ng; ++g) {
+      const uint32_t nst = (M->g_dim[g] + 3) / 4;
+      reinterpret_cast<uint32_t*>(smem + kGmeta)[M->g_bits[g] - 1] =
+          (1u << 31) | static_cast<uint32_t>(M->bitoff[M->g_pos[g]]) | (nst << 10) | (slot << 16) |
+          (static_cast<uint32_t>(g) << 20);
+      slot += (nst + 15) / 16;
+    }
+  }
+  __syncthreads();
+  // ---- the Q-side rotation (Sec. 4): qr[h][p] = (Pi_g q_g)_j / sqrt(d_g d_h)
+  // at stream position p = g_pos[g] + j.  Staged in LDS before the tables
+  // are built: qg[h][p] = q_h[dim(p)] (the queries gathered into stream
+  // order), qr, then every group's rotation (transposed, sum_g d_g^2 <= 128^2
+  // floats) loaded with coalesced reads, so the dot products read only LDS.
+  static_assert(2 * 8 * kHeadDim * 4 + kHeadDim * kHeadDim * 4 <= kQimg + kQimgBytes, "rotation staging");
+  static_assert(2 * 8 * kHeadDim * 4 <= kQimg, "qr must survive the query image build");
+  float* qg = reinterpret_cast<float*>(smem);      // [G][128]
+  float* qr = qg + 8 * kHeadDim;                   // [G][128]
+  float* rs = qr + 8 * kHeadDim;                   // staged rotations
+  {
+    const size_t qoff = (static_cast<size_t>(lz) * hqn + kvh * G) * kHeadDim;
+    for (int i = tid; i < G * kHeadDim; i += kThreads) {
+      const int h = i >> 7, p = i & 127;
+      qg[i] = ld_q(q, qoff + h * kHeadDim + M->dim[p], d.in_dtype);
+    }
+    const float* rotkt = reinterpret_cast<const float*>(blob + kOffRotKT);
+    int off = 0;
+    for (int g = 0; g < ng; ++g) {
+      const int dg = M->g_dim[g];
+      const float* rt = rotkt + rotk_index(dg);
+      for (int i = tid; i < dg * dg; i += kThreads) rs[off + i] = rt[i];
+      off += dg * dg;
+    }
+  }
+  __syncthreads();
+  {
+    int off = 0;
+    for (int g = 0; g < ng; ++g) {
+      const int dg = M->g_dim[g], p0 = M->g_pos[g];
+      const float* rt = rs + off;  // Pi_dg transposed: rt[k dg + j] = Pi[j][k]
+      for (int i = tid; i < G * dg; i += kThreads) {
+        const int h = i / dg, j = i - h * dg;
+        float acc = 0.f;
+        for (int k = 0; k < dg; ++k) acc = fmaf(rt[k * dg + j], qg[h * kHeadDim + p0 + k], acc);
+        qr[h * kHeadDim + p0 + j] = acc / sqrtf(static_cast<float>(dg) * kHeadDim);
+      }
+      off += dg * dg;
+    }
+  }
+  __syncthreads();
+  // ---- query image: slot s, lane 4b+i holds step 16(s - slot0_g) + b of
+  // group g, head i of each set, 4 coordinates, as fp16 hi and lo parts
+  {
+    for (int g = 0; g < ng; ++g) {
+      const uint32_t meta = lds32(smem, kGmeta + 4 * (M->g_bits[g] - 1));
+      const int nst = gm_steps(meta), slot0 = gm_slot(meta);
+      const int gpos = M->g_pos[g], gdim = M->g_dim[g];
+      const int nchunk = (nst + 15) / 16;
+      for (int i = tid; i < nchunk * NSET * 64 * 4; i += kThreads) {
+        const int k = i & 3, l = (i >> 2) & 63, set = (i >> 8) % NSET, ch = (i >> 8) / NSET;
+        const int step = 16 * ch + (l >> 2), qh = 4 * set + (l & 3), coord = 4 * step + k;
+        float v = 0.f;
+        if (step < nst && coord < gdim && qh < G) v = qr[qh * kHeadDim + gpos + coord];
+        const _Float16 hi = static_cast<_Float16>(v);
+        const _Float16 lo = static_cast<_Float16>(v - static_cast<float>(hi));
+        uint8_t* dst = smem + kQimg + ((((slot0 + ch) * 2 + set) * 2) * 64 + l) * 8 + k * 2;
+        *reinterpret_cast<_Float16*>(dst) = hi;
+        *reinterpret_cast<_Float16*>(dst + 64 * 8) = lo;
+      }
+    }
+  }
+  __syncthreads();
   // ---- lookup tables
   for (int i = tid; i < 16 * 16; i += kThreads) {
     const int e = i >> 4;
@@ -475,42 +558,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     const int b = i < 64 ? 6 : (i < 192 ? 7 : 8);
     const int k = i < 64 ? i : (i < 192 ? i - 64 : i - 192);
     *reinterpret_cast<uint16_t*>(smem + kLutF + i * 2) = c16[cb_index(b) + k];
-  }
-  // ---- group metadata by width; each group's steps start a new query slot
-  if (tid < 8) reinterpret_cast<uint32_t*>(smem + kGmeta)[tid] = 0u;
-  __syncthreads();
-  if (tid == 0) {
-    uint32_t slot = 0;
-    for (int g = 0; g < ng; ++g) {
-      const uint32_t nst = (M->g_dim[g] + 3) / 4;
-      reinterpret_cast<uint32_t*>(smem + kGmeta)[M->g_bits[g] - 1] =
-          (1u << 31) | static_cast<uint32_t>(M->bitoff[M->g_pos[g]]) | (nst << 10) | (slot << 16) |
-          (static_cast<uint32_t>(g) << 20);
-      slot += (nst + 15) / 16;
-    }
-  }
-  __syncthreads();
-  // ---- query image: slot s, lane 4b+i holds step 16(s - slot0_g) + b of
-  // group g, head i of each set, 4 coordinates, as fp16 hi and lo parts
-  {
-    const float* qbase = qp + (static_cast<size_t>(lz) * hqn + kvh * G) * kHeadDim;
-    for (int g = 0; g < ng; ++g) {
-      const uint32_t meta = lds32(smem, kGmeta + 4 * (M->g_bits[g] - 1));
-      const int nst = gm_steps(meta), slot0 = gm_slot(meta);
-      const int gpos = M->g_pos[g], gdim = M->g_dim[g];
-      const int nchunk = (nst + 15) / 16;
-      for (int i = tid; i < nchunk * NSET * 64 * 4; i += kThreads) {
-        const int k = i & 3, l = (i >> 2) & 63, set = (i >> 8) % NSET, ch = (i >> 8) / NSET;
-        const int step = 16 * ch + (l >> 2), q = 4 * set + (l & 3), coord = 4 * step + k;
-        float v = 0.f;
-        if (step < nst && coord < gdim && q < G) v = qbase[q * kHeadDim + gpos + coord];
-        const _Float16 hi = static_cast<_Float16>(v);
-        const _Float16 lo = static_cast<_Float16>(v - static_cast<float>(hi));
-        uint8_t* dst = smem + kQimg + ((((slot0 + ch) * 2 + set) * 2) * 64 + l) * 8 + k * 2;
-        *reinterpret_cast<_Float16*>(dst) = hi;
-        *reinterpret_cast<_Float16*>(dst + 64 * 8) = lo;
-      }
-    }
   }
   __syncthreads();
 
@@ -630,38 +677,88 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
       for (int r = 0; r < 4; ++r) fo[(wave * 8 + s * 4 + r) * kHeadDim + 64 * h + lane] = O[s][h][r];
   }
   __syncthreads();
+  float* os = fo + kWaves * 8 * kHeadDim;  // [G][128] merged output, rotated V domain
   for (int i = tid; i < G * kHeadDim; i += kThreads) {
-    const int q = i >> 7, dd = i & 127;
+    const int qh = i >> 7, dd = i & 127;
     float mx = kNegInf;
-    for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, fm[w * 8 + q]);
+    for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, fm[w * 8 + qh]);
     float l = 0.f, a = 0.f;
     if (mx != kNegInf) {
       for (int w = 0; w < kWaves; ++w) {
-        const float mw = fm[w * 8 + q];
+        const float mw = fm[w * 8 + qh];
         if (mw == kNegInf) continue;
         const float e = __expf(mw - mx);
-        l = fmaf(fl[w * 8 + q], e, l);
-        a = fmaf(fo[(w * 8 + q) * kHeadDim + dd], e, a);
+        l = fmaf(fl[w * 8 + qh], e, l);
+        a = fmaf(fo[(w * 8 + qh) * kHeadDim + dd], e, a);
       }
     }
-    float* pb = part + ((static_cast<size_t>(lz) * hqn + kvh * G + q) * n_splits + split) * 130;
-    pb[2 + dd] = a;
-    if (dd == 0) {
-      pb[0] = mx;
-      pb[1] = l;
+    if (n_splits == 1) {
+      os[i] = l > 0.f ? a / l : 0.f;
+    } else {
+      // device-coherent stores (no L2 write-back needed before the counter)
+      float* pb = part + ((static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits + split) * 130;
+      __hip_atomic_store(pb + 2 + dd, a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (dd == 0) {
+        __hip_atomic_store(pb, mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(pb + 1, l, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
+  }
+
+  // ---------------- merge the splits (exact log-sum-exp) in the workgroup
+  // that finishes last; it resets the counter for the next call
+  if (n_splits > 1) {
+    // Every thread's partial stores complete (device-coherent) before the
+    // barrier; then one increment per workgroup.  The increment's return
+    // value gates the loads below, so they cannot run ahead of it.
+    int* last = reinterpret_cast<int*>(smem + kGmeta);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __syncthreads();
+    if (tid == 0)
+      *last = __hip_atomic_fetch_add(counters + lz * d.n_kv + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+              n_splits - 1;
+    __syncthreads();
+    if (*last == 0) return;
+    for (int i = tid; i < G * kHeadDim; i += kThreads) {
+      const int qh = i >> 7, dd = i & 127;
+      const float* P = part + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits * 130;
+      const auto ld = [](const float* x) { return __hip_atomic_load(x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
+      float mx = kNegInf;
+      for (int sp = 0; sp < n_splits; ++sp) mx = fmaxf(mx, ld(P + sp * 130));
+      float l = 0.f, a = 0.f;
+      if (mx != kNegInf) {
+        for (int sp = 0; sp < n_splits; ++sp) {
+          const float ms = ld(P + sp * 130);
+          if (ms == kNegInf) continue;
+          const float e = __expf(ms - mx);
+          l = fmaf(ld(P + sp * 130 + 1), e, l);
+          a = fmaf(ld(P + sp * 130 + 2 + dd), e, a);
+        }
+      }
+      os[i] = l > 0.f ? a / l : 0.f;
+    }
+    if (tid == 0) __hip_atomic_store(counters + lz * d.n_kv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  // ---------------- back from the rotated V domain: out = Pi_V^T o
+  const float* rotv = reinterpret_cast<const float*>(blob + kOffRotV);
+  for (int i = tid; i < G * kHeadDim; i += kThreads) {
+    const int qh = i >> 7, dd = i & 127;
+    float r = 0.f;
+    for (int jj = 0; jj < kHeadDim; ++jj) r = fmaf(rotv[jj * kHeadDim + dd], os[qh * kHeadDim + jj], r);
+    out[(static_cast<size_t>(lz) * hqn + kvh * G + qh) * kHeadDim + dd] = r;
   }
 }
 
-// Launch the split pass for value width BV (one instantiation per file).
+// Launch the packed decode for value width BV (one instantiation per file).
 template <int BV>
-hipError_t launch_split_bv_impl(const Dims& d, const void* layout, const int32_t* ctx_len, const CachePtrs& c,
-                                const DecodeWs& ws, hipStream_t s) {
+hipError_t launch_split_bv_impl(const Dims& d, const void* layout, const void* q, const int32_t* ctx_len,
+                                const CachePtrs& c, float* out, const DecodeWs& ws, hipStream_t s) {
   dim3 grid(ws.n_splits, d.n_kv, d.batch * d.n_lc);
   const uint8_t* blob = static_cast<const uint8_t*>(layout);
   const auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, d, blob, ctx_len, c, ws.qp, ws.part, ws.n_splits,
-                       ws.split_len);
+    hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, d, blob, q, ctx_len, c, out, ws.counters, ws.part,
+                       ws.n_splits, ws.split_len);
   };
   if (d.group <= 4) {
     if (d.k_words <= 8) go(k_split_mfma<1, 8, BV>);

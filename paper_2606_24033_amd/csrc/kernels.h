@@ -25,17 +25,18 @@ hipError_t launch_quantize_append(const Dims& d, const void* layout, const void*
 
 // Workspace carve-up of one decode call.
 struct DecodeWs {
-  float* qp;        // [n_lc][batch][Hq][128] rotated, scaled queries
-  float* part;      // [n_lc][batch][Hq][n_splits][130] (m, l, acc[128])
-  int n_splits;     // splits actually launched
-  int split_len;    // tokens per split, multiple of 32
+  int32_t* counters;  // [n_lc][batch][n_kv] finished-split counters (zero between calls)
+  float* part;        // [n_lc][batch][Hq][n_splits][130] (m, l, acc[128])
+  int n_splits;       // splits actually launched
+  int split_len;      // tokens per split, multiple of 64
 };
 
-// Split pass of the packed decode (decode_impl.h), one entry per value code
-// width (decode_bv1.hip .. decode_bv8.hip); each writes ws.part.
-#define BGTQ_DECL_SPLIT(N)                                                                              \
-  hipError_t launch_split_bv##N(const Dims& d, const void* layout, const int32_t* ctx_len, const CachePtrs& c, \
-                                const DecodeWs& ws, hipStream_t s);
+// Packed decode (decode_impl.h), one entry per value code width
+// (decode_bv1.hip .. decode_bv8.hip): query rotation, split pass and the
+// merge of the splits in a single kernel.
+#define BGTQ_DECL_SPLIT(N)                                                                                \
+  hipError_t launch_split_bv##N(const Dims& d, const void* layout, const void* q, const int32_t* ctx_len, \
+                                const CachePtrs& c, float* out, const DecodeWs& ws, hipStream_t s);
 BGTQ_DECL_SPLIT(1)
 BGTQ_DECL_SPLIT(2)
 BGTQ_DECL_SPLIT(3)

@@ -2,8 +2,7 @@
 //
 //  k_quantize      : TQ-MSE encode (Sec. 2.2) of appended K rows per same-rate
 //                    group (end of Sec. 3.2) and of V rows, dense b-bit pack.
-//  k_qrot          : Q-side rotation of the decode queries (Sec. 4).
-//  (the split pass over the packed cache lives in decode_impl.h)
+//  (the packed-cache decode lives in decode_impl.h)
 //  k_merge         : exact log-sum-exp merge of the splits + inverse V rotation.
 //  k_split_fp16    : the same decode over an fp16 cache (comparator).
 #include <hip/hip_fp16.h>
@@ -179,34 +178,6 @@ __global__ __launch_bounds__(256) void k_quantize(Dims d, const uint8_t* __restr
 }
 
 // ---------------------------------------------------------------------------
-// Q-side rotation: q'_p = (Pi_g q_g)_j / (sqrt(d_g) sqrt(d_h)) for stream
-// position p = g_pos[g] + j.  One workgroup per (query head, sequence, layer).
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(128) void k_qrot(Dims d, const uint8_t* __restrict__ blob,
-                                              const void* __restrict__ q, float* __restrict__ qp) {
-  __shared__ float qs[kHeadDim];
-  const int tid = threadIdx.x;
-  const int hq = blockIdx.x, seq = blockIdx.y, lc = blockIdx.z;
-  const int layer = d.layer >= 0 ? d.layer : lc;
-  const int hqn = d.n_kv * d.group;
-  const int kvh = hq / d.group;
-  const size_t qoff = ((static_cast<size_t>(lc) * d.batch + seq) * hqn + hq) * kHeadDim;
-  qs[tid] = ld_in(q, qoff + tid, d.in_dtype);
-  const float* rotkt = reinterpret_cast<const float*>(blob + kOffRotKT);
-  const RowMeta* M = reinterpret_cast<const RowMeta*>(blob + kOffRows) + (layer * d.n_kv + kvh);
-  __syncthreads();
-  for (int g = 0; g < M->n_groups; ++g) {
-    const int dg = M->g_dim[g], p0 = M->g_pos[g];
-    if (tid < dg) {
-      const float* rt = rotkt + rotk_index(dg);
-      float acc = 0.f;
-      for (int i = 0; i < dg; ++i) acc = fmaf(rt[i * dg + tid], qs[M->dim[p0 + i]], acc);
-      qp[qoff + p0 + tid] = acc / sqrtf(static_cast<float>(dg) * kHeadDim);
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
 // fp16 comparator: same split structure over an uncompressed fp16 cache.
 // ---------------------------------------------------------------------------
 template <int G>
@@ -364,25 +335,16 @@ hipError_t launch_quantize_append(const Dims& d, const void* layout, const void*
 hipError_t launch_decode_packed(const Dims& d, const void* layout, const void* q,
                                 const int32_t* ctx_len, const CachePtrs& c, float* out,
                                 const DecodeWs& ws, hipStream_t s) {
-  const uint8_t* blob = static_cast<const uint8_t*>(layout);
-  const int hqn = d.n_kv * d.group;
-  hipLaunchKernelGGL(k_qrot, dim3(hqn, d.batch, d.n_lc), dim3(128), 0, s, d, blob, q, ws.qp);
-  hipError_t e;
   switch (d.v_bits) {
-    case 1: e = launch_split_bv1(d, layout, ctx_len, c, ws, s); break;
-    case 2: e = launch_split_bv2(d, layout, ctx_len, c, ws, s); break;
-    case 3: e = launch_split_bv3(d, layout, ctx_len, c, ws, s); break;
-    case 4: e = launch_split_bv4(d, layout, ctx_len, c, ws, s); break;
-    case 5: e = launch_split_bv5(d, layout, ctx_len, c, ws, s); break;
-    case 6: e = launch_split_bv6(d, layout, ctx_len, c, ws, s); break;
-    case 7: e = launch_split_bv7(d, layout, ctx_len, c, ws, s); break;
-    default: e = launch_split_bv8(d, layout, ctx_len, c, ws, s); break;
+    case 1: return launch_split_bv1(d, layout, q, ctx_len, c, out, ws, s);
+    case 2: return launch_split_bv2(d, layout, q, ctx_len, c, out, ws, s);
+    case 3: return launch_split_bv3(d, layout, q, ctx_len, c, out, ws, s);
+    case 4: return launch_split_bv4(d, layout, q, ctx_len, c, out, ws, s);
+    case 5: return launch_split_bv5(d, layout, q, ctx_len, c, out, ws, s);
+    case 6: return launch_split_bv6(d, layout, q, ctx_len, c, out, ws, s);
+    case 7: return launch_split_bv7(d, layout, q, ctx_len, c, out, ws, s);
+    default: return launch_split_bv8(d, layout, q, ctx_len, c, out, ws, s);
   }
-  if (e != hipSuccess) return e;
-  const float* rotv = reinterpret_cast<const float*>(blob + kOffRotV);
-  hipLaunchKernelGGL(k_merge, dim3(hqn, d.batch, d.n_lc), dim3(128), 0, s, d, ws.part, ws.n_splits,
-                     rotv, out);
-  return hipGetLastError();
 }
 
 template <int G>
