@@ -231,27 +231,50 @@ constexpr int kRowPad = 4;  // zero words after a key row: a sub-chunk reads wor
 template <int B>
 constexpr int qk_nw() { return (qk_ch<B>() * 4 * B + 31) / 32; }  // words per sub-chunk
 
-// Steps K..min(mm, KEND)-1 of a sub-chunk, in windows of 4: first every
-// table lookup of the window, then its MFMAs (query block K0 + step), so the
-// lookups overlap each other.
-template <int B, int K, int KEND, int N>
-__device__ __forceinline__ void qk_dec(const uint8_t* smem, const uint32_t (&aw)[N], int mm, const LaneRep& rep,
-                                       half4_t (&kv)[4]) {
-  kv[K & 3] = decode4<B, 4 * B * K>(smem, aw, rep);
-  if constexpr (K + 1 < KEND) {
-    if (mm > K + 1) qk_dec<B, K + 1, KEND, N>(smem, aw, mm, rep, kv);
-  }
-}
-template <int NSET, int K0, int K, int KEND>
-__device__ __forceinline__ void qk_mac(const half4_t (&kv)[4], int mm, const half4_t (&qh)[NSET],
-                                       const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
+// One MFMA pair (hi and lo query parts) of query block K.
+template <int NSET, int K>
+__device__ __forceinline__ void qk_mac(const half4_t& kv, const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
+                                       float4_t (&acc)[NSET]) {
 #pragma unroll
   for (int s = 0; s < NSET; ++s) {
-    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(qh[s], kv[K & 3], acc[s], 4, K0 + K, 0);
-    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(ql[s], kv[K & 3], acc[s], 4, K0 + K, 0);
+    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(qh[s], kv, acc[s], 4, K, 0);
+    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(ql[s], kv, acc[s], 4, K, 0);
   }
-  if constexpr (K + 1 < KEND) {
-    if (mm > K + 1) qk_mac<NSET, K0, K + 1, KEND>(kv, mm, qh, ql, acc);
+}
+
+// Window W (steps 4W..4W+3) of a sub-chunk whose first step uses query
+// block K0; steps >= mm do not exist.  For b <= 4 the four lookups are
+// issued unconditionally (a step past the group end decodes other bits of
+// the row or its zero padding: a valid table index, whose MFMA is skipped),
+// so the decoded operands need no merge copies; wider codes take four
+// lookups a step and are decoded only when the step exists.
+template <int B, int NSET, int K0, int W, int N>
+__device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&aw)[N], int mm, const LaneRep& rep,
+                                          const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
+                                          float4_t (&acc)[NSET]) {
+  constexpr int k = 4 * W;
+  if constexpr (B <= 4) {
+    const half4_t kv0 = decode4<B, 4 * B * (k + 0)>(smem, aw, rep);
+    const half4_t kv1 = decode4<B, 4 * B * (k + 1)>(smem, aw, rep);
+    const half4_t kv2 = decode4<B, 4 * B * (k + 2)>(smem, aw, rep);
+    const half4_t kv3 = decode4<B, 4 * B * (k + 3)>(smem, aw, rep);
+    qk_mac<NSET, K0 + k>(kv0, qh, ql, acc);
+    if (mm > k + 1) {
+      qk_mac<NSET, K0 + k + 1>(kv1, qh, ql, acc);
+      if (mm > k + 2) {
+        qk_mac<NSET, K0 + k + 2>(kv2, qh, ql, acc);
+        if (mm > k + 3) qk_mac<NSET, K0 + k + 3>(kv3, qh, ql, acc);
+      }
+    }
+  } else {
+    qk_mac<NSET, K0 + k>(decode4<B, 4 * B * k>(smem, aw, rep), qh, ql, acc);
+    if (mm > k + 1) {
+      qk_mac<NSET, K0 + k + 1>(decode4<B, 4 * B * (k + 1)>(smem, aw, rep), qh, ql, acc);
+      if (mm > k + 2) {
+        qk_mac<NSET, K0 + k + 2>(decode4<B, 4 * B * (k + 2)>(smem, aw, rep), qh, ql, acc);
+        if (mm > k + 3) qk_mac<NSET, K0 + k + 3>(decode4<B, 4 * B * (k + 3)>(smem, aw, rep), qh, ql, acc);
+      }
+    }
   }
 }
 
@@ -270,14 +293,9 @@ __device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t
     for (int i = 0; i < NW; ++i) aw[i] = __builtin_amdgcn_alignbit(rw[w0 + i + 1], rw[w0 + i], sh);
     aw[NW] = 0;
     const int mm = min(CH, ms - SC * CH);
-    half4_t kv[4];
-    qk_dec<B, 0, 4, NW + 1>(smem, aw, mm, rep, kv);
-    qk_mac<NSET, SC * CH, 0, 4>(kv, mm, qh, ql, acc);
+    qk_window<B, NSET, SC * CH, 0, NW + 1>(smem, aw, mm, rep, qh, ql, acc);
     if constexpr (CH == 8) {
-      if (mm > 4) {
-        qk_dec<B, 4, 8, NW + 1>(smem, aw, mm, rep, kv);
-        qk_mac<NSET, SC * CH, 4, 8>(kv, mm, qh, ql, acc);
-      }
+      if (mm > 4) qk_window<B, NSET, SC * CH, 1, NW + 1>(smem, aw, mm, rep, qh, ql, acc);
     }
   }
 }
@@ -589,18 +607,29 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   int t0 = t_begin + wave * 64;
   const RowPtrs R{c.k_codes + row * cap * kw, c.k_norms + row * kMaxGroups * cap,
                   c.v_codes + row * (cap / kTile) * kHeadDim * BV, c.v_norms + row * cap};
-  uint32_t rw[KWB + kRowPad], knp[4], rw2[KWB], knp2[4], vw[4][pv_words<BV>()];
-  uint2 vn;
+  // keys and values of the next tile are in flight while a tile is computed
+  uint32_t rw[KWB + kRowPad], knp[4], rw2[KWB], knp2[4], vw[4][pv_words<BV>()], vw2[4][pv_words<BV>()];
+  uint2 vn, vn2;
 #pragma unroll
   for (int i = KWB; i < KWB + kRowPad; ++i) rw[i] = 0u;
-  if (t0 < t_end) load_keys<KWB>(rw2, knp2, gmb, R, cap, kw, t0, lane);
+  if (t0 < t_end) {
+    load_keys<KWB>(rw2, knp2, gmb, R, cap, kw, t0, lane);
+    load_values<BV>(vn2, vw2, R, t0, lane);
+  }
   for (; t0 < t_end; t0 += stride) {
 #pragma unroll
     for (int i = 0; i < KWB; ++i) rw[i] = rw2[i];
 #pragma unroll
     for (int p = 0; p < 4; ++p) knp[p] = knp2[p];
-    load_values<BV>(vn, vw, R, t0, lane);
-    if (t0 + stride < t_end) load_keys<KWB>(rw2, knp2, gmb, R, cap, kw, t0 + stride, lane);
+#pragma unroll
+    for (int th = 0; th < 4; ++th)
+#pragma unroll
+      for (int w = 0; w < pv_words<BV>(); ++w) vw[th][w] = vw2[th][w];
+    vn = vn2;
+    if (t0 + stride < t_end) {
+      load_keys<KWB>(rw2, knp2, gmb, R, cap, kw, t0 + stride, lane);
+      load_values<BV>(vn2, vw2, R, t0 + stride, lane);
+    }
     const int tk = t0 + lane;
     {
       // Re-read the width metadata every tile (through an opaque address):
