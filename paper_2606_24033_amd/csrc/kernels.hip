@@ -96,7 +96,58 @@ __global__ __launch_bounds__(256) void k_quantize(Dims d, const uint8_t* __restr
   __syncthreads();
 
   const int wave = tid >> 6, lane = tid & 63;
-  for (int s = wave; s < kTile; s += 4) {
+  if (t_hi - t_lo <= 4) {
+    // Few tokens (a decode-step append): all four waves work on one token at
+    // a time.  Norms: wave w sums groups w, w+4 and wave 3 the value row, in
+    // the same order as the per-wave path below; rotations: thread p < 128
+    // takes key stream position p, thread 128 + j value coordinate j.  Same
+    // arithmetic as the per-wave path, so the codes are the same.
+    __shared__ float gnrm[kMaxGroups + 1];
+    const int ng = meta.n_groups;
+    for (int t = t_lo; t < t_hi; ++t) {
+      const int s = t - tile * kTile;
+      for (int g = wave; g < ng; g += 4) {
+        const int dg = meta.g_dim[g], p0 = meta.g_pos[g];
+        float ss = 0.f;
+        for (int i = lane; i < dg; i += 64) {
+          const float x = xk[s][meta.dim[p0 + i]];
+          ss = fmaf(x, x, ss);
+        }
+        ss = wave_sum(ss);
+        if (lane == 0) gnrm[g] = sqrtf(ss);
+      }
+      if (wave == 3) {
+        float ss = 0.f;
+        for (int i = lane; i < kHeadDim; i += 64) ss = fmaf(xv[s][i], xv[s][i], ss);
+        ss = wave_sum(ss);
+        if (lane == 0) gnrm[kMaxGroups] = sqrtf(ss);
+      }
+      __syncthreads();
+      if (tid < kHeadDim) {
+        const int p = tid, g = meta.grp[p];
+        const int b = meta.g_bits[g], dg = meta.g_dim[g], p0 = meta.g_pos[g], j = p - p0;
+        const float nrm = gnrm[g];
+        const float scale = nrm > 0.f ? sqrtf(static_cast<float>(dg)) / nrm : 0.f;
+        const float* rt = rotkt + rotk_index(dg);
+        float acc = 0.f;
+#pragma unroll 16
+        for (int i = 0; i < dg; ++i) acc = fmaf(rt[i * dg + j], xk[s][meta.dim[p0 + i]], acc);
+        ck[s][p] = static_cast<uint8_t>(scalar_code(thr + thr_index(b), b, acc * scale));
+        if (j == 0) c.k_norms[(row * kMaxGroups + g) * d.capacity + t] = __half_as_ushort(__float2half_rn(nrm));
+      } else {
+        const int j = tid - kHeadDim, b = d.v_bits;
+        const float nrm = gnrm[kMaxGroups];
+        const float scale = nrm > 0.f ? sqrtf(static_cast<float>(kHeadDim)) / nrm : 0.f;
+        float acc = 0.f;
+#pragma unroll 16
+        for (int i = 0; i < kHeadDim; ++i) acc = fmaf(rotvt[i * kHeadDim + j], xv[s][i], acc);
+        cv[s][j] = static_cast<uint8_t>(scalar_code(thr + thr_index(b), b, acc * scale));
+        if (j == 0) c.v_norms[row * d.capacity + t] = __half_as_ushort(__float2half_rn(nrm));
+      }
+      __syncthreads();
+    }
+  }
+  for (int s = wave; s < kTile && t_hi - t_lo > 4; s += 4) {
     const int t = tile * kTile + s;
     if (t < t_lo || t >= t_hi) continue;
     for (int g = 0; g < meta.n_groups; ++g) {

@@ -290,3 +290,52 @@ def test_argument_errors_on_device():
         bad = np.array(st.bits)
         bad[0, 0, 0] += 1
         bg.Layout(st.cfg, bad, synth.flat_rot_k(st.rot_k), st.rot_v)
+
+
+def test_llama_128k_step_sampled():
+    """Full-size step in the launch configuration bench.py times: Llama-3.1-8B
+    shape (32 layers, 8 KV heads, G = 4, base 5e5, bf16, K2V2), 131072 cached
+    rows, one all-layer append of row 131072 and one all-layer decode with the
+    default split plan for bench.py's max_ctx.  Sampled (layer, KV head) pairs
+    are checked in full against the oracle fed the same bf16 inputs: every
+    code and norm of their 131073 rows and the attention of their 4 query heads."""
+    bg = bgm()
+    T, L, H, G = 131072, 32, 8, 4
+    max_ctx = T + 25                    # bench.py default: 5 warm-up + 20 timed steps
+    st = P.make_setup(3, L, 1, H, G, T + 64, 128, 2, 5e5, "bf16", n_cal=2048)
+    layout, cache = build(st)
+    samples = [(5, 3), (27, 6)]
+    kept = {}
+    knew = torch.empty((L, 1, 1, H, 128), dtype=torch.bfloat16, device="cuda")
+    vnew = torch.empty_like(knew)
+    wp0 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for layer in range(L):
+        sig = np.stack([st.sigma[layer, h] for h in range(H)])
+        k, v = synth.torch_layer_kv(st.seed, layer, T + 1, sig, st.base)
+        bg.blockgtq_quantize_append(st.cfg, layout, layer, k[None, :T].contiguous(), v[None, :T].contiguous(), wp0,
+                                    cache)
+        knew[layer, 0, 0] = k[T]
+        vnew[layer, 0, 0] = v[T]
+        for sl, sh in samples:
+            if sl == layer:
+                kept[sl, sh] = (k[:, sh].float().cpu().numpy(), v[:, sh].float().cpu().numpy())
+        del k, v
+    log("llama 128k: prefill done")
+    q = torch.stack([synth.torch_queries(st.seed, layer, H * G, [T], st.base)[0] for layer in range(L)])[:, None]
+    q = q.contiguous()
+    bg.blockgtq_quantize_append(st.cfg, layout, -1, knew, vnew, torch.tensor([T], dtype=torch.int32, device="cuda"),
+                                cache)
+    out = bg.blockgtq_decode_attn(st.cfg, layout, -1, q, torch.tensor([T + 1], dtype=torch.int32, device="cuda"),
+                                  max_ctx, cache)
+    out = out.cpu().numpy().astype(np.float64)
+    qh = q.float().cpu().numpy()
+    stats = P.Stats()
+    for layer, head in samples:
+        k, v = kept[layer, head]
+        rows = P.oracle_rows(st, layer, head, k, v)
+        check_cache(st, cache, layer, 0, head, rows, T + 1, stats, f"llama L{layer} h{head}")
+        ref = P.oracle_attention(st, layer, head, qh[layer, 0, head * G:(head + 1) * G], rows, T + 1)
+        err = P.rel_err(out[layer, 0, head * G:(head + 1) * G], ref)
+        log("llama 128k layer", layer, "head", head, "rel err", err, "ties", vars(stats))
+        assert err <= P.tol_attention()
+    assert stats.code_ties <= 1e-4 * stats.codes
