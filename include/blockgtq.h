@@ -27,8 +27,11 @@
  *            ascending bit width, inside a group the rotated coordinates in
  *            order; each code is a dense b-bit field, LSB first; stream bit o
  *            is bit (o % 32) of word (o / 32).  k_words = ceil(2 B / 32).
- *  k_norms : fp16  [n_layers][batch][n_kv_heads][8][capacity]
- *            The radius of each same-rate group (group ordinal, ascending b).
+ *  k_norms : fp16  [n_layers][batch][n_kv_heads][capacity * 8]
+ *            Token-major radii: with n_g same-rate groups in the (layer, KV
+ *            head) and S = n_g rounded up to even, token t's group radii sit
+ *            at [t*S, t*S + n_g) in group ordinal (ascending b) order, so one
+ *            4/8/12/16-byte load reads a token's radii.  Slots past n_g stay 0.
  *  v_codes : uint32 [n_layers][batch][n_kv_heads][capacity/32][d_h][b_v]
  *            Tiles of 32 tokens.  For rotated coordinate j the 32 codes of a
  *            tile form one 32*b_v-bit string; token slot s = t % 32 occupies

@@ -186,7 +186,7 @@ class Cache:
         import torch
         L, B, H, C = cfg.n_layers, cfg.batch, cfg.n_kv_heads, cfg.capacity
         self.k_codes = torch.zeros((L, B, H, C, cfg.k_words), dtype=torch.int32, device=device)
-        self.k_norms = torch.zeros((L, B, H, MAX_GROUPS, C), dtype=torch.float16, device=device)
+        self.k_norms = torch.zeros((L, B, H, C * MAX_GROUPS), dtype=torch.float16, device=device)
         self.v_codes = torch.zeros((L, B, H, C // 32, HEAD_DIM, cfg.v_bits), dtype=torch.int32, device=device)
         self.v_norms = torch.zeros((L, B, H, C), dtype=torch.float16, device=device)
 

@@ -215,9 +215,10 @@ SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested
   if (requested > 0) {
     n = std::min(requested, max_splits);
   } else {
-    // about four 8-wave workgroups per CU, each split at least 512 rows long
+    // about two 8-wave workgroups per CU (one round on 256 CUs: each pays
+    // its prologue once), each split at least 512 rows long
     const long units = static_cast<long>(c->n_kv_heads) * c->batch * n_lc;
-    n = static_cast<int>((1024 + units - 1) / units);
+    n = static_cast<int>((512 + units - 1) / units);
     n = std::max(1, std::min(n, (max_ctx + 511) / 512));
   }
   p.split_len = ((max_ctx + n - 1) / n + 63) / 64 * 64;

@@ -359,29 +359,35 @@ __device__ __forceinline__ void pv_steps(std::integer_sequence<int, S...>, const
 }
 
 // ---------------------------------------------------------------- loads
+// Load of a T at a 32-bit byte offset from a wave-uniform base (the global
+// load form with a scalar base and a 32-bit vector offset).
+template <class T>
+__device__ __forceinline__ T ld_at(const void* base, uint32_t byte_off) {
+  return *reinterpret_cast<const T*>(static_cast<const char*>(base) + byte_off);
+}
+
 // Cache rows of one (layer, sequence, KV head).
 struct RowPtrs {
   const uint32_t* k;   // [cap][kw] key rows
-  const uint16_t* kn;  // [8][cap] group radii
+  const uint16_t* kn;  // [cap][S] group radii, S = n_g rounded up to even
   const uint32_t* v;   // [cap / 32][128][BV] value tiles
   const uint16_t* vn;  // [cap] value radii
 };
 
 // Key data of the 64-token tile at t0 (loaded one tile ahead of its use):
-// rw[0..kw) = the key row of token t0 + lane (zero up to KWB), knp[(b - 1) / 2] half
-// (b - 1) & 1 = that token's radius in the width-b group.  Every token of a
+// rw[0..kw) = the key row of token t0 + lane (zero up to KWB), knp[g / 2]
+// half g & 1 = that token's radius of group ordinal g.  Every token of a
 // tile is below the capacity (a multiple of 64).
 template <int KWB>
-__device__ __forceinline__ void load_keys(uint32_t (&rw)[KWB], uint32_t (&knp)[4],
-                                          const uint32_t (&gmb)[8], const RowPtrs& R, int cap, int kw, int t0,
-                                          int lane) {
+__device__ __forceinline__ void load_keys(uint32_t (&rw)[KWB], uint32_t (&knp)[4], int nslot, const RowPtrs& R,
+                                          int kw, int t0, int lane) {
   const uint32_t* src = R.k + static_cast<size_t>(t0) * kw;
-  const uint32_t lo = static_cast<uint32_t>(lane * kw);
+  const uint32_t lo = static_cast<uint32_t>(lane * kw * 4);
   if ((kw & 3) == 0) {
 #pragma unroll
     for (int i = 0; i < KWB; i += 4) {
       if (i < kw) {
-        const uint4 v = *reinterpret_cast<const uint4*>(src + lo + i);
+        const uint4 v = ld_at<uint4>(src, lo + 4 * i);
         rw[i] = v.x;
         rw[i + 1] = v.y;
         rw[i + 2] = v.z;
@@ -392,16 +398,17 @@ __device__ __forceinline__ void load_keys(uint32_t (&rw)[KWB], uint32_t (&knp)[4
     }
   } else {
 #pragma unroll
-    for (int i = 0; i < KWB; ++i) rw[i] = i < kw ? src[lo + i] : 0u;
+    for (int i = 0; i < KWB; ++i) rw[i] = i < kw ? ld_at<uint32_t>(src, lo + 4 * i) : 0u;
   }
-  const uint16_t* nb = R.kn + t0;
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    uint32_t lo16 = 0, hi16 = 0;
-    if (gmb[2 * p] >> 31) lo16 = nb[static_cast<size_t>(gm_plane(gmb[2 * p])) * cap + lane];
-    if (gmb[2 * p + 1] >> 31) hi16 = nb[static_cast<size_t>(gm_plane(gmb[2 * p + 1])) * cap + lane];
-    knp[p] = lo16 | (hi16 << 16);
-  }
+  const uint16_t* nb = R.kn + static_cast<size_t>(t0) * nslot;
+  const uint32_t lo2 = static_cast<uint32_t>(lane * nslot * 2);
+  // one 16-byte window per token (slots past n_g belong to the next token and
+  // are never used; the window stays inside the row's capacity * 8 slots)
+  const uint4 x = ld_at<uint4>(nb, lo2);
+  knp[0] = x.x;
+  knp[1] = x.y;
+  knp[2] = x.z;
+  knp[3] = x.w;
 }
 
 // Value data of the tile at t0 (loaded when the tile starts, used after its
@@ -410,16 +417,16 @@ __device__ __forceinline__ void load_keys(uint32_t (&rw)[KWB], uint32_t (&knp)[4
 template <int BV>
 __device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][pv_words<BV>()], const RowPtrs& R, int t0,
                                             int lane) {
-  vn = *reinterpret_cast<const uint2*>(R.vn + t0 + 4 * (lane >> 2));
+  vn = ld_at<uint2>(R.vn + t0, static_cast<uint32_t>(8 * (lane >> 2)));
   const uint32_t* vb = R.v + static_cast<size_t>(t0 / kTile) * kHeadDim * BV;
-  const uint32_t lo = static_cast<uint32_t>(lane * BV);
+  const uint32_t lo = static_cast<uint32_t>(lane * BV * 4);
 #pragma unroll
   for (int th = 0; th < 4; ++th) {
-    const uint32_t* src = vb + ((th >> 1) * kHeadDim + 64 * (th & 1)) * BV + lo;
+    const uint32_t* src = vb + ((th >> 1) * kHeadDim + 64 * (th & 1)) * BV;
     if constexpr (BV % 4 == 0) {
 #pragma unroll
       for (int w = 0; w < BV; w += 4) {
-        const uint4 v4 = *reinterpret_cast<const uint4*>(src + w);
+        const uint4 v4 = ld_at<uint4>(src, lo + 4 * w);
         vw[th][w] = v4.x;
         vw[th][w + 1] = v4.y;
         vw[th][w + 2] = v4.z;
@@ -428,15 +435,22 @@ __device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][pv_word
     } else if constexpr (BV % 2 == 0) {
 #pragma unroll
       for (int w = 0; w < BV; w += 2) {
-        const uint2 v2 = *reinterpret_cast<const uint2*>(src + w);
+        const uint2 v2 = ld_at<uint2>(src, lo + 4 * w);
         vw[th][w] = v2.x;
         vw[th][w + 1] = v2.y;
       }
     } else {
 #pragma unroll
-      for (int w = 0; w < BV; ++w) vw[th][w] = src[w];
+      for (int w = 0; w < BV; ++w) vw[th][w] = ld_at<uint32_t>(src, lo + 4 * w);
     }
   }
+}
+
+// Radius bits of group ordinal g (wave-uniform) from the packed halves.
+__device__ __forceinline__ uint32_t radius_bits(const uint32_t (&knp)[4], int g) {
+  const int i = g >> 1;
+  const uint32_t w = i == 0 ? knp[0] : (i == 1 ? knp[1] : (i == 2 ? knp[2] : knp[3]));
+  return (w >> (16 * (g & 1))) & 0xFFFFu;
 }
 
 // QK of one tile over every present width.
@@ -444,8 +458,8 @@ template <int NSET, int KWB, int... BM1>
 __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const uint8_t* smem,
                                        const uint32_t (&rw)[KWB + kRowPad], const uint32_t (&knp)[4],
                                        const uint32_t (&gmb)[8], const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
-  ((gmb[BM1] >> 31 ? qk_group<BM1 + 1, NSET, KWB>(smem, rw, gmb[BM1], (knp[BM1 / 2] >> (16 * (BM1 & 1))) & 0xFFFFu,
-                                                  rep, lane, L)
+  ((gmb[BM1] >> 31 ? qk_group<BM1 + 1, NSET, KWB>(smem, rw, gmb[BM1], radius_bits(knp, gm_plane(gmb[BM1])), rep,
+                                                  lane, L)
                    : void()),
    ...);
 }
@@ -605,6 +619,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   // while the current one is computed.
   const int stride = kWaves * 64;
   int t0 = t_begin + wave * 64;
+  const int nslot = (ng + 1) & ~1;  // radius slots per token
   const RowPtrs R{c.k_codes + row * cap * kw, c.k_norms + row * kMaxGroups * cap,
                   c.v_codes + row * (cap / kTile) * kHeadDim * BV, c.v_norms + row * cap};
   // keys and values of the next tile are in flight while a tile is computed
@@ -613,7 +628,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
 #pragma unroll
   for (int i = KWB; i < KWB + kRowPad; ++i) rw[i] = 0u;
   if (t0 < t_end) {
-    load_keys<KWB>(rw2, knp2, gmb, R, cap, kw, t0, lane);
+    load_keys<KWB>(rw2, knp2, nslot, R, kw, t0, lane);
     load_values<BV>(vn2, vw2, R, t0, lane);
   }
   for (; t0 < t_end; t0 += stride) {
@@ -627,7 +642,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
       for (int w = 0; w < pv_words<BV>(); ++w) vw[th][w] = vw2[th][w];
     vn = vn2;
     if (t0 + stride < t_end) {
-      load_keys<KWB>(rw2, knp2, gmb, R, cap, kw, t0 + stride, lane);
+      load_keys<KWB>(rw2, knp2, nslot, R, kw, t0 + stride, lane);
       load_values<BV>(vn2, vw2, R, t0 + stride, lane);
     }
     const int tk = t0 + lane;

@@ -133,7 +133,7 @@ __global__ __launch_bounds__(256) void k_quantize(Dims d, const uint8_t* __restr
 #pragma unroll 16
         for (int i = 0; i < dg; ++i) acc = fmaf(rt[i * dg + j], xk[s][meta.dim[p0 + i]], acc);
         ck[s][p] = static_cast<uint8_t>(scalar_code(thr + thr_index(b), b, acc * scale));
-        if (j == 0) c.k_norms[(row * kMaxGroups + g) * d.capacity + t] = __half_as_ushort(__float2half_rn(nrm));
+        if (j == 0) c.k_norms[row * kMaxGroups * d.capacity + t * ((ng + 1) & ~1) + g] = __half_as_ushort(__float2half_rn(nrm));
       } else {
         const int j = tid - kHeadDim, b = d.v_bits;
         const float nrm = gnrm[kMaxGroups];
@@ -166,7 +166,9 @@ __global__ __launch_bounds__(256) void k_quantize(Dims d, const uint8_t* __restr
         for (int i = 0; i < dg; ++i) acc = fmaf(rt[i * dg + j], xk[s][meta.dim[p0 + i]], acc);
         ck[s][p0 + j] = static_cast<uint8_t>(scalar_code(thr + thr_index(b), b, acc * scale));
       }
-      if (lane == 0) c.k_norms[(row * kMaxGroups + g) * d.capacity + t] = __half_as_ushort(__float2half_rn(nrm));
+      if (lane == 0)
+        c.k_norms[row * kMaxGroups * d.capacity + t * ((meta.n_groups + 1) & ~1) + g] =
+            __half_as_ushort(__float2half_rn(nrm));
     }
     {
       const int b = d.v_bits;

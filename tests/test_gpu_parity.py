@@ -73,7 +73,8 @@ def check_cache(st, cache, layer, seq, head, rows, T, stats, what):
     else:
         stats.codes += rows.kcodes[:T].size
     ng = rows.knorms.shape[1]
-    kn = cache.k_norms[layer, seq, head, :ng, :T].cpu().numpy().T
+    S = ng + (ng & 1)   # token-major radii, n_g rounded up to even per token
+    kn = cache.k_norms[layer, seq, head, :T * S].cpu().numpy().reshape(T, S)[:, :ng]
     P.compare_norms(kn, rows.knorms[:T], rows.kexact[:T], 128, stats, what + " K norms")
     vt = cache.v_codes[layer, seq, head].cpu().numpy().view(np.uint32)
     vc = P.read_value_codes(vt, st.cfg.v_bits, T)
