@@ -215,11 +215,11 @@ SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested
   if (requested > 0) {
     n = std::min(requested, max_splits);
   } else {
-    // about two 8-wave workgroups per CU (one round on 256 CUs: each pays
-    // its prologue once), each split at least 512 rows long
+    // about one 16-wave workgroup per CU (one round on 256 CUs: each pays
+    // its prologue once), each split at least 1024 rows (a tile per wave)
     const long units = static_cast<long>(c->n_kv_heads) * c->batch * n_lc;
-    n = static_cast<int>((512 + units - 1) / units);
-    n = std::max(1, std::min(n, (max_ctx + 511) / 512));
+    n = static_cast<int>((256 + units - 1) / units);
+    n = std::max(1, std::min(n, (max_ctx + 1023) / 1024));
   }
   p.split_len = ((max_ctx + n - 1) / n + 63) / 64 * 64;
   p.n_splits = (max_ctx + p.split_len - 1) / p.split_len;

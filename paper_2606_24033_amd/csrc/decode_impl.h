@@ -3,8 +3,8 @@
 // products -> online softmax over a split of the key axis, then the exact
 // log-sum-exp merge of the splits and the inverse V rotation).
 //
-// Work mapping.  One workgroup = 8 waves = one (split, KV head, sequence[,
-// layer]).  A wave owns 64-token tiles (two value tiles).  Both products run
+// Work mapping.  One workgroup = 16 waves (one per CU) = one (split, KV
+// head, sequence[, layer]).  A wave owns 64-token tiles (two value tiles).  Both products run
 // on 4x4x4 f16 MFMA instructions (16 independent 4x4 blocks) whose A operand
 // is broadcast from one block (CBSZ = 4, ABID = the block), so the operand
 // shared by all 64 lanes is held once per 16 steps instead of once per step:
@@ -51,24 +51,29 @@ namespace split_detail {
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 8;
+constexpr int kWaves = 16;  // one workgroup per CU: 160 KB of LDS for the tables
 constexpr int kThreads = kWaves * 64;
 constexpr int kMaxSlots = 10;  // 16-step query slots of one key row: sum_g ceil(steps_g / 16)
 constexpr float kNegInf = -__builtin_huge_valf();
 
-// LDS map (bytes).  Entry strides: 128 B for the 16- and 32-replica tables,
-// 32 B for the 8-replica b = 4 table, 2 B for the plain b >= 6 tables.
-constexpr int kLut1 = 0;                        // b=1: 16 entries (4 codes) x 16 replicas x 8 B
-constexpr int kLut2 = kLut1 + 16 * 16 * 8;      // b=2: 256 (4 codes) x 16 x 8
-constexpr int kLut3 = kLut2 + 256 * 16 * 8;     // b=3: 64 (2 codes) x 32 x 4
+// LDS map (bytes).  The b = 2 table has 32 replicas at a 256-byte entry
+// stride: the lanes of a half-wave read 32 distinct banks, and the address is
+// one byte permute of (code byte, replica offset).  Other entry strides: 128 B
+// for the 16- and 32-replica tables, 32 B for the 8-replica b = 4 table, 2 B
+// for the plain b >= 6 tables.
+constexpr int kLut2 = 0;                        // b=2: 256 entries (4 codes) x 32 replicas x 8 B
+constexpr int kLut1 = kLut2 + 256 * 256;        // b=1: 16 entries (4 codes) x 16 replicas x 8 B
+constexpr int kLut3 = kLut1 + 16 * 16 * 8;      // b=3: 64 (2 codes) x 32 x 4
 constexpr int kLut4 = kLut3 + 64 * 32 * 4;      // b=4: 256 (2 codes) x 8 x 4
 constexpr int kLut5 = kLut4 + 256 * 8 * 4;      // b=5: 32 (1 code, low half) x 32 x 4
 constexpr int kLutF = kLut5 + 32 * 32 * 4;      // b=6,7,8: plain fp16 tables at +0, +128, +384
 constexpr int kQimg = kLutF + 1024;             // [slot][set][hi,lo][lane] x 8 B
 constexpr int kQimgBytes = kMaxSlots * 2 * 2 * 64 * 8;
 constexpr int kGmeta = kQimg + kQimgBytes;      // [b - 1] packed group metadata
-constexpr int kLdsBytes = kGmeta + 64;
-static_assert(kLdsBytes <= 80 * 1024, "two workgroups per CU");
+constexpr int kCbStage = kGmeta + 64;           // fp16 codebooks, staged for the table build
+constexpr int kLdsBytes = kCbStage + 2 * 512;
+static_assert(2 * kCodebookEntries <= 2 * 512, "codebook staging");
+static_assert(kLdsBytes <= 160 * 1024, "one workgroup per CU");
 
 // Packed group metadata, indexed by width: bit 31 present, bits 0..9 first
 // stream bit, 10..15 steps, 16..19 first query slot, 20..22 radius plane.
@@ -196,15 +201,28 @@ struct LaneRep {
   uint32_t r16;  // (lane & 15) * 8
   uint32_t r32;  // (lane & 31) * 4
   uint32_t r8;   // (lane & 7) * 4
+  uint32_t r2;   // (lane & 31) * 8: replica offset in the b = 2 table
 };
+
+// Byte K of w (a compile-time byte) as the entry index of the b = 2 table:
+// one permute builds entry * 256 + replica.
+template <int K>
+__device__ __forceinline__ uint32_t lut2_addr(uint32_t w, uint32_t r2) {
+  return __builtin_amdgcn_perm(w, r2, 0x0C0C0000u | ((4u + K) << 8));
+}
 
 // Four consecutive B-bit codes starting at bit POS of w -> four fp16
 // centroids (an MFMA operand).
 template <int B, int POS, int N>
 __device__ __forceinline__ half4_t decode4(const uint8_t* smem, const uint32_t (&w)[N], const LaneRep& r) {
-  if constexpr (B <= 2) {
-    constexpr int base = B == 1 ? kLut1 : kLut2;
-    const uint2 u = lds64(smem, base + r.r16 + (field<POS, 4 * B>(w) << 7));
+  if constexpr (B == 2 && POS % 8 == 0) {
+    const uint2 u = lds64(smem, kLut2 + lut2_addr<(POS % 32) / 8>(w[POS / 32], r.r2));
+    return as_half4(u.x, u.y);
+  } else if constexpr (B == 2) {
+    const uint2 u = lds64(smem, kLut2 + r.r2 + (field<POS, 8>(w) << 8));
+    return as_half4(u.x, u.y);
+  } else if constexpr (B == 1) {
+    const uint2 u = lds64(smem, kLut1 + r.r16 + (field<POS, 4>(w) << 7));
     return as_half4(u.x, u.y);
   } else if constexpr (B == 3) {
     return as_half4(lds32(smem, kLut3 + r.r32 + (field<POS, 6>(w) << 7)),
@@ -254,10 +272,14 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
                                           float4_t (&acc)[NSET]) {
   constexpr int k = 4 * W;
   if constexpr (B <= 4) {
-    const half4_t kv0 = decode4<B, 4 * B * (k + 0)>(smem, aw, rep);
-    const half4_t kv1 = decode4<B, 4 * B * (k + 1)>(smem, aw, rep);
-    const half4_t kv2 = decode4<B, 4 * B * (k + 2)>(smem, aw, rep);
-    const half4_t kv3 = decode4<B, 4 * B * (k + 3)>(smem, aw, rep);
+    half4_t kv0 = decode4<B, 4 * B * (k + 0)>(smem, aw, rep);
+    half4_t kv1 = decode4<B, 4 * B * (k + 1)>(smem, aw, rep);
+    half4_t kv2 = decode4<B, 4 * B * (k + 2)>(smem, aw, rep);
+    half4_t kv3 = decode4<B, 4 * B * (k + 3)>(smem, aw, rep);
+    // keep the four lookups ahead of the guarded products (one LDS round
+    // trip per window): without this the compiler sinks each lookup into
+    // the branch that uses it and serialises them
+    asm volatile("" : "+v"(kv0), "+v"(kv1), "+v"(kv2), "+v"(kv3));
     qk_mac<NSET, K0 + k>(kv0, qh, ql, acc);
     if (mm > k + 1) {
       qk_mac<NSET, K0 + k + 1>(kv1, qh, ql, acc);
@@ -483,58 +505,87 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   const int ng = M->n_groups;
 
   // ---- group metadata by width; each group's steps start a new query slot
-  if (tid < 8) reinterpret_cast<uint32_t*>(smem + kGmeta)[tid] = 0u;
-  __syncthreads();
   if (tid == 0) {
+    uint32_t* gmw = reinterpret_cast<uint32_t*>(smem + kGmeta);
+    for (int b = 0; b < 8; ++b) gmw[b] = 0u;
     uint32_t slot = 0;
     for (int g = 0; g < ng; ++g) {
       const uint32_t nst = (M->g_dim[g] + 3) / 4;
-      reinterpret_cast<uint32_t*>(smem + kGmeta)[M->g_bits[g] - 1] =
-          (1u << 31) | static_cast<uint32_t>(M->bitoff[M->g_pos[g]]) | (nst << 10) | (slot << 16) |
-          (static_cast<uint32_t>(g) << 20);
+      gmw[M->g_bits[g] - 1] = (1u << 31) | static_cast<uint32_t>(M->bitoff[M->g_pos[g]]) | (nst << 10) |
+                              (slot << 16) | (static_cast<uint32_t>(g) << 20);
       slot += (nst + 15) / 16;
     }
   }
-  __syncthreads();
   // ---- the Q-side rotation (Sec. 4): qr[h][p] = (Pi_g q_g)_j / sqrt(d_g d_h)
   // at stream position p = g_pos[g] + j.  Staged in LDS before the tables
   // are built: qg[h][p] = q_h[dim(p)] (the queries gathered into stream
-  // order), qr, then every group's rotation (transposed, sum_g d_g^2 <= 128^2
-  // floats) loaded with coalesced reads, so the dot products read only LDS.
+  // order), qr, every group's rotation (transposed, one block after the
+  // other: sum_g d_g^2 <= 128^2 floats) and the codebooks.  All global reads
+  // of the set-up are issued together, before the first one is used.
   static_assert(2 * 8 * kHeadDim * 4 + kHeadDim * kHeadDim * 4 <= kQimg + kQimgBytes, "rotation staging");
   static_assert(2 * 8 * kHeadDim * 4 <= kQimg, "qr must survive the query image build");
+  static_assert(8 * kHeadDim <= kThreads, "one query coordinate per thread");
+  constexpr int kRotPerThread = kHeadDim * kHeadDim / kThreads;
   float* qg = reinterpret_cast<float*>(smem);      // [G][128]
   float* qr = qg + 8 * kHeadDim;                   // [G][128]
   float* rs = qr + 8 * kHeadDim;                   // staged rotations
+  uint16_t* cbs = reinterpret_cast<uint16_t*>(smem + kCbStage);
+  // per-group rotation blocks: staged offset, size, first stream position
+  int roff[kMaxGroups], rdim[kMaxGroups], rpos[kMaxGroups];
+  int rtot = 0;
+#pragma unroll
+  for (int g = 0; g < kMaxGroups; ++g) {
+    rdim[g] = g < ng ? M->g_dim[g] : 0;
+    rpos[g] = g < ng ? M->g_pos[g] : kHeadDim;
+    roff[g] = rtot;
+    rtot += rdim[g] * rdim[g];
+  }
   {
-    const size_t qoff = (static_cast<size_t>(lz) * hqn + kvh * G) * kHeadDim;
-    for (int i = tid; i < G * kHeadDim; i += kThreads) {
-      const int h = i >> 7, p = i & 127;
-      qg[i] = ld_q(q, qoff + h * kHeadDim + M->dim[p], d.in_dtype);
-    }
     const float* rotkt = reinterpret_cast<const float*>(blob + kOffRotKT);
-    int off = 0;
-    for (int g = 0; g < ng; ++g) {
-      const int dg = M->g_dim[g];
-      const float* rt = rotkt + rotk_index(dg);
-      for (int i = tid; i < dg * dg; i += kThreads) rs[off + i] = rt[i];
-      off += dg * dg;
+    const size_t qoff = (static_cast<size_t>(lz) * hqn + kvh * G) * kHeadDim;
+    const bool has_q = tid < G * kHeadDim;
+    const float qv = has_q ? ld_q(q, qoff + (tid >> 7) * kHeadDim + M->dim[tid & 127], d.in_dtype) : 0.f;
+    const uint32_t cv = tid < kCodebookEntries ? c16[tid] : 0u;
+    float rv[kRotPerThread];
+#pragma unroll
+    for (int u = 0; u < kRotPerThread; ++u) {
+      const int i = tid + u * kThreads;
+      rv[u] = 0.f;
+      if (u * kThreads < rtot && i < rtot) {
+        int src = rotk_index(rdim[0]) + i;  // element i of the staged blocks in the source layout
+#pragma unroll
+        for (int g = 1; g < kMaxGroups; ++g)
+          if (g < ng && i >= roff[g]) src = rotk_index(rdim[g]) + (i - roff[g]);
+        rv[u] = rotkt[src];
+      }
     }
+    if (has_q) qg[tid] = qv;
+    if (tid < kCodebookEntries) cbs[tid] = static_cast<uint16_t>(cv);
+#pragma unroll
+    for (int u = 0; u < kRotPerThread; ++u)
+      if (u * kThreads < rtot && tid + u * kThreads < rtot) rs[tid + u * kThreads] = rv[u];
   }
   __syncthreads();
-  {
-    int off = 0;
-    for (int g = 0; g < ng; ++g) {
-      const int dg = M->g_dim[g], p0 = M->g_pos[g];
-      const float* rt = rs + off;  // Pi_dg transposed: rt[k dg + j] = Pi[j][k]
-      for (int i = tid; i < G * dg; i += kThreads) {
-        const int h = i / dg, j = i - h * dg;
-        float acc = 0.f;
-        for (int k = 0; k < dg; ++k) acc = fmaf(rt[k * dg + j], qg[h * kHeadDim + p0 + k], acc);
-        qr[h * kHeadDim + p0 + j] = acc / sqrtf(static_cast<float>(dg) * kHeadDim);
+  if (tid < G * kHeadDim) {
+    // one rotated coordinate per thread: p = stream position, g its group
+    const int h = tid >> 7, p = tid & 127;
+    int dg = rdim[0], off = roff[0], p0 = rpos[0];
+#pragma unroll
+    for (int g = 1; g < kMaxGroups; ++g)
+      if (p >= rpos[g]) {
+        dg = rdim[g];
+        off = roff[g];
+        p0 = rpos[g];
       }
-      off += dg * dg;
+    const int j = p - p0;
+    const float* rt = rs + off;  // Pi_dg transposed: rt[k dg + j] = Pi[j][k]
+    const float* qq = qg + h * kHeadDim + p0;
+    float a0 = 0.f, a1 = 0.f;
+    for (int k = 0; k < dg; k += 2) {  // d_g is even
+      a0 = fmaf(rt[k * dg + j], qq[k], a0);
+      a1 = fmaf(rt[(k + 1) * dg + j], qq[k + 1], a1);
     }
+    qr[tid] = (a0 + a1) / sqrtf(static_cast<float>(dg) * kHeadDim);
   }
   __syncthreads();
   // ---- query image: slot s, lane 4b+i holds step 16(s - slot0_g) + b of
@@ -562,34 +613,34 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   // ---- lookup tables
   for (int i = tid; i < 16 * 16; i += kThreads) {
     const int e = i >> 4;
-    const uint16_t* cb = c16 + cb_index(1);
+    const uint16_t* cb = cbs + cb_index(1);
     *reinterpret_cast<uint2*>(smem + kLut1 + i * 8) =
         make_uint2(cb[e & 1] | (static_cast<uint32_t>(cb[(e >> 1) & 1]) << 16),
                    cb[(e >> 2) & 1] | (static_cast<uint32_t>(cb[(e >> 3) & 1]) << 16));
   }
-  for (int i = tid; i < 256 * 16; i += kThreads) {
-    const int e = i >> 4;
-    const uint16_t* cb = c16 + cb_index(2);
+  for (int i = tid; i < 256 * 32; i += kThreads) {
+    const int e = i >> 5;
+    const uint16_t* cb = cbs + cb_index(2);
     *reinterpret_cast<uint2*>(smem + kLut2 + i * 8) =
         make_uint2(cb[e & 3] | (static_cast<uint32_t>(cb[(e >> 2) & 3]) << 16),
                    cb[(e >> 4) & 3] | (static_cast<uint32_t>(cb[(e >> 6) & 3]) << 16));
   }
   for (int i = tid; i < 64 * 32; i += kThreads) {
     const int e = i >> 5;
-    const uint16_t* cb = c16 + cb_index(3);
+    const uint16_t* cb = cbs + cb_index(3);
     *reinterpret_cast<uint32_t*>(smem + kLut3 + i * 4) = cb[e & 7] | (static_cast<uint32_t>(cb[(e >> 3) & 7]) << 16);
   }
   for (int i = tid; i < 256 * 8; i += kThreads) {
     const int e = i >> 3;
-    const uint16_t* cb = c16 + cb_index(4);
+    const uint16_t* cb = cbs + cb_index(4);
     *reinterpret_cast<uint32_t*>(smem + kLut4 + i * 4) = cb[e & 15] | (static_cast<uint32_t>(cb[e >> 4]) << 16);
   }
   for (int i = tid; i < 32 * 32; i += kThreads)
-    *reinterpret_cast<uint32_t*>(smem + kLut5 + i * 4) = c16[cb_index(5) + (i >> 5)];
+    *reinterpret_cast<uint32_t*>(smem + kLut5 + i * 4) = cbs[cb_index(5) + (i >> 5)];
   for (int i = tid; i < 64 + 128 + 256; i += kThreads) {
     const int b = i < 64 ? 6 : (i < 192 ? 7 : 8);
     const int k = i < 64 ? i : (i < 192 ? i - 64 : i - 192);
-    *reinterpret_cast<uint16_t*>(smem + kLutF + i * 2) = c16[cb_index(b) + k];
+    *reinterpret_cast<uint16_t*>(smem + kLutF + i * 2) = cbs[cb_index(b) + k];
   }
   __syncthreads();
 
@@ -597,7 +648,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
 #pragma unroll
   for (int b = 0; b < 8; ++b) gmb[b] = __builtin_amdgcn_readfirstlane(lds32(smem, kGmeta + 4 * b));
   const LaneRep rep{static_cast<uint32_t>(lane & 15) * 8u, static_cast<uint32_t>(lane & 31) * 4u,
-                    static_cast<uint32_t>(lane & 7) * 4u};
+                    static_cast<uint32_t>(lane & 7) * 4u, static_cast<uint32_t>(lane & 31) * 8u};
 
   const int ctx = min(ctx_len[seq], cap);
   const int t_begin = split * split_len;
@@ -622,29 +673,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   const int nslot = (ng + 1) & ~1;  // radius slots per token
   const RowPtrs R{c.k_codes + row * cap * kw, c.k_norms + row * kMaxGroups * cap,
                   c.v_codes + row * (cap / kTile) * kHeadDim * BV, c.v_norms + row * cap};
-  // keys and values of the next tile are in flight while a tile is computed
-  uint32_t rw[KWB + kRowPad], knp[4], rw2[KWB], knp2[4], vw[4][pv_words<BV>()], vw2[4][pv_words<BV>()];
-  uint2 vn, vn2;
+  // the next tile's keys are in flight while a tile is computed; its values
+  // are loaded when it starts and used after its QK products
+  uint32_t rw[KWB + kRowPad], knp[4], rw2[KWB], knp2[4], vw[4][pv_words<BV>()];
+  uint2 vn;
 #pragma unroll
   for (int i = KWB; i < KWB + kRowPad; ++i) rw[i] = 0u;
-  if (t0 < t_end) {
-    load_keys<KWB>(rw2, knp2, nslot, R, kw, t0, lane);
-    load_values<BV>(vn2, vw2, R, t0, lane);
-  }
+  if (t0 < t_end) load_keys<KWB>(rw2, knp2, nslot, R, kw, t0, lane);
   for (; t0 < t_end; t0 += stride) {
 #pragma unroll
     for (int i = 0; i < KWB; ++i) rw[i] = rw2[i];
 #pragma unroll
     for (int p = 0; p < 4; ++p) knp[p] = knp2[p];
-#pragma unroll
-    for (int th = 0; th < 4; ++th)
-#pragma unroll
-      for (int w = 0; w < pv_words<BV>(); ++w) vw[th][w] = vw2[th][w];
-    vn = vn2;
-    if (t0 + stride < t_end) {
-      load_keys<KWB>(rw2, knp2, nslot, R, kw, t0 + stride, lane);
-      load_values<BV>(vn2, vw2, R, t0 + stride, lane);
-    }
+    load_values<BV>(vn, vw, R, t0, lane);
+    if (t0 + stride < t_end) load_keys<KWB>(rw2, knp2, nslot, R, kw, t0 + stride, lane);
     const int tk = t0 + lane;
     {
       // Re-read the width metadata every tile (through an opaque address):
@@ -767,17 +809,37 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
       const int qh = i >> 7, dd = i & 127;
       const float* P = part + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits * 130;
       const auto ld = [](const float* x) { return __hip_atomic_load(x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
-      float mx = kNegInf;
-      for (int sp = 0; sp < n_splits; ++sp) mx = fmaxf(mx, ld(P + sp * 130));
-      float l = 0.f, a = 0.f;
-      if (mx != kNegInf) {
-        for (int sp = 0; sp < n_splits; ++sp) {
-          const float ms = ld(P + sp * 130);
-          if (ms == kNegInf) continue;
-          const float e = __expf(ms - mx);
-          l = fmaf(ld(P + sp * 130 + 1), e, l);
-          a = fmaf(ld(P + sp * 130 + 2 + dd), e, a);
+      // eight splits per round, their loads in flight together; running
+      // maximum with rescaling between rounds
+      float mx = kNegInf, l = 0.f, a = 0.f;
+      for (int sp0 = 0; sp0 < n_splits; sp0 += 8) {
+        float ms[8], ls[8], as[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          ms[u] = kNegInf;
+          ls[u] = as[u] = 0.f;
+          if (sp0 + u < n_splits) {
+            const float* ps = P + (sp0 + u) * 130;
+            ms[u] = ld(ps);
+            ls[u] = ld(ps + 1);
+            as[u] = ld(ps + 2 + dd);
+          }
         }
+        float mc = mx;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) mc = fmaxf(mc, ms[u]);
+        if (mc == kNegInf) continue;
+        const float r = mx == kNegInf ? 0.f : __expf(mx - mc);
+        l *= r;
+        a *= r;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (ms[u] == kNegInf) continue;
+          const float e = __expf(ms[u] - mc);
+          l = fmaf(ls[u], e, l);
+          a = fmaf(as[u], e, a);
+        }
+        mx = mc;
       }
       os[i] = l > 0.f ? a / l : 0.f;
     }
