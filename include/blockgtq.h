@@ -119,9 +119,10 @@ int blockgtq_codebook(int32_t b, uint16_t* h_c16_out, float* h_thr_out);
 int blockgtq_layout_bytes(const bgtq_config* cfg, size_t* bytes_out);
 int blockgtq_cache_bytes(const bgtq_config* cfg, size_t* k_codes, size_t* k_norms,
                          size_t* v_codes, size_t* v_norms);
-/* Workspace of one blockgtq_decode_attn call: n_layers_in_call = 1 for a
- * single layer, cfg->n_layers for layer = -1.  n_splits as passed to the
- * call (0 = the heuristic for max_ctx).  The workspace starts with one int32
+/* Workspace of one blockgtq_decode_attn (or _fp16) call: n_layers_in_call =
+ * 1 for a single layer, cfg->n_layers for layer = -1.  n_splits as passed to
+ * the call (0 = the heuristic for max_ctx, which differs between the two
+ * entry points; the size returned covers either).  The workspace starts with one int32
  * counter per (layer in call, sequence, KV head) that the kernel uses to find
  * the last split to finish: it must be zero-filled once before its first
  * use, and every completed call leaves it zero again.  Calls that share a

@@ -207,7 +207,13 @@ struct SplitPlan {
   int n_splits, split_len;
 };
 
-SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested) {
+// Default split counts: the packed decode runs one 16-wave workgroup per CU
+// (each pays its prologue once), each split at least 1024 rows (a 64-row tile
+// per wave); the fp16 comparator runs 4-wave workgroups and wants about eight
+// per CU, each split at least 256 rows.
+enum class Kernel { kPacked, kFp16 };
+
+SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested, Kernel k = Kernel::kPacked) {
   SplitPlan p;
   if (max_ctx <= 0) return {1, 64};
   const int max_splits = (max_ctx + kTile - 1) / kTile;
@@ -215,11 +221,11 @@ SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested
   if (requested > 0) {
     n = std::min(requested, max_splits);
   } else {
-    // about one 16-wave workgroup per CU (one round on 256 CUs: each pays
-    // its prologue once), each split at least 1024 rows (a tile per wave)
     const long units = static_cast<long>(c->n_kv_heads) * c->batch * n_lc;
-    n = static_cast<int>((256 + units - 1) / units);
-    n = std::max(1, std::min(n, (max_ctx + 1023) / 1024));
+    const long wgs = k == Kernel::kPacked ? 256 : 2048;
+    const int min_len = k == Kernel::kPacked ? 1024 : 256;
+    n = static_cast<int>((wgs + units - 1) / units);
+    n = std::max(1, std::min(n, (max_ctx + min_len - 1) / min_len));
   }
   p.split_len = ((max_ctx + n - 1) / n + 63) / 64 * 64;
   p.n_splits = (max_ctx + p.split_len - 1) / p.split_len;
@@ -338,7 +344,10 @@ int blockgtq_workspace_bytes(const bgtq_config* cfg, int32_t n_layers_in_call, i
     return fail(BGTQ_EINVAL, "n_layers_in_call must be 1 or n_layers");
   if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);
   if (max_ctx < 0 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [0, capacity]", max_ctx);
-  *bytes_out = ws_bytes_of(cfg, n_layers_in_call, plan_splits(cfg, n_layers_in_call, max_ctx, n_splits));
+  // enough for either decode entry point
+  *bytes_out = std::max(ws_bytes_of(cfg, n_layers_in_call, plan_splits(cfg, n_layers_in_call, max_ctx, n_splits)),
+                        ws_bytes_of(cfg, n_layers_in_call,
+                                    plan_splits(cfg, n_layers_in_call, max_ctx, n_splits, Kernel::kFp16)));
   return ok();
 }
 
@@ -478,14 +487,14 @@ int blockgtq_quantize_append(const bgtq_config* cfg, const void* d_layout, int32
 
 static int check_decode_args(const bgtq_config* cfg, int32_t layer, const void* d_q, const int32_t* d_ctx_len,
                              int32_t max_ctx, float* d_out, void* d_ws, size_t ws_bytes, int32_t n_splits,
-                             DecodeWs* ws) {
+                             DecodeWs* ws, Kernel kern) {
   if (int e = check_cfg(cfg)) return e;
   if (!d_q || !d_ctx_len || !d_out || !d_ws) return fail(BGTQ_EINVAL, "NULL pointer");
   if (layer < -1 || layer >= cfg->n_layers) return fail(BGTQ_EINVAL, "layer %d out of range", layer);
   if (max_ctx < 0 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [0, capacity]", max_ctx);
   if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);
   const int n_lc = layer < 0 ? cfg->n_layers : 1;
-  const SplitPlan p = plan_splits(cfg, n_lc, max_ctx, n_splits);
+  const SplitPlan p = plan_splits(cfg, n_lc, max_ctx, n_splits, kern);
   const size_t need = ws_bytes_of(cfg, n_lc, p);
   if (ws_bytes < need) return fail(BGTQ_EWORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
   ws->counters = static_cast<int32_t*>(d_ws);
@@ -499,7 +508,8 @@ int blockgtq_decode_attn(const bgtq_config* cfg, const void* d_layout, int32_t l
                          const int32_t* d_ctx_len, int32_t max_ctx, const bgtq_cache* cache, float* d_out,
                          void* d_workspace, size_t ws_bytes, int32_t n_splits, void* stream) {
   DecodeWs ws;
-  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws))
+  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws,
+                                Kernel::kPacked))
     return e;
   if (!d_layout || !cache || !cache->k_codes || !cache->k_norms || !cache->v_codes || !cache->v_norms)
     return fail(BGTQ_EINVAL, "NULL pointer");
@@ -515,7 +525,8 @@ int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void*
                               int32_t max_ctx, const void* d_k16, const void* d_v16, float* d_out,
                               void* d_workspace, size_t ws_bytes, int32_t n_splits, void* stream) {
   DecodeWs ws;
-  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws))
+  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws,
+                                Kernel::kFp16))
     return e;
   if (!d_k16 || !d_v16) return fail(BGTQ_EINVAL, "NULL pointer");
   hipError_t e = launch_decode_fp16(dims_of(cfg, layer), d_q, d_ctx_len, d_k16, d_v16, d_out, ws,
