@@ -172,7 +172,8 @@ int blockgtq_quantize_append(const bgtq_config* cfg, const void* d_layout, int32
  * (max, sum, accumulator) states are merged exactly by log-sum-exp.  The
  * query is rotated into each group's code domain first (the Q-side rotation).
  * d_q: post-RoPE queries in cfg->in_dtype, [batch][n_kv_heads*group][head_dim]
- *      (layer >= 0) or [n_layers][batch][...][head_dim] (layer == -1).
+ *      (layer >= 0) or [n_layers][batch][...][head_dim] (layer == -1);
+ *      4-byte aligned (EINVAL otherwise).
  * d_ctx_len: int32 [batch], each in [0, max_ctx]; a sequence with 0 rows
  *      gets an all-zero output.
  * max_ctx: host-side upper bound of d_ctx_len (<= capacity), sizes the splits.
@@ -180,7 +181,9 @@ int blockgtq_quantize_append(const bgtq_config* cfg, const void* d_layout, int32
  * d_workspace / ws_bytes: see blockgtq_workspace_bytes (EWORKSPACE if short;
  *      zero-filled before first use).  One kernel launch: the query rotation,
  *      the split pass and the merge of the splits.
- * n_splits: 0 = heuristic, else 1 .. 4096. */
+ * n_splits: 0 = heuristic, else 1 .. 4096.  The (sequence, KV head, split)
+ *      workgroups are dispatched in the layout's order of estimated row cost,
+ *      most expensive first; the result does not depend on the order. */
 int blockgtq_decode_attn(const bgtq_config* cfg, const void* d_layout, int32_t layer,
                          const void* d_q, const int32_t* d_ctx_len, int32_t max_ctx,
                          const bgtq_cache* cache, float* d_out, void* d_workspace,

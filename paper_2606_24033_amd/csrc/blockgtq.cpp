@@ -207,8 +207,9 @@ struct SplitPlan {
   int n_splits, split_len;
 };
 
-// Default split counts: the packed decode runs one 16-wave workgroup per CU
-// (each pays its prologue once), each split at least 1024 rows (a 64-row tile
+// Default split counts: the packed decode runs one 16-wave workgroup per CU at
+// a time, two rounds (the second round's workgroups go to the CUs that finish
+// first, so the work evens out), each split at least 1024 rows (a 64-row tile
 // per wave); the fp16 comparator runs 4-wave workgroups and wants about eight
 // per CU, each split at least 256 rows.
 enum class Kernel { kPacked, kFp16 };
@@ -222,7 +223,7 @@ SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested
     n = std::min(requested, max_splits);
   } else {
     const long units = static_cast<long>(c->n_kv_heads) * c->batch * n_lc;
-    const long wgs = k == Kernel::kPacked ? 256 : 2048;
+    const long wgs = k == Kernel::kPacked ? 512 : 2048;
     const int min_len = k == Kernel::kPacked ? 1024 : 256;
     n = static_cast<int>((wgs + units - 1) / units);
     n = std::max(1, std::min(n, (max_ctx + min_len - 1) / min_len));
@@ -371,6 +372,8 @@ int blockgtq_layout_init(const bgtq_config* cfg, const uint8_t* h_k_bits, const 
   H->off_rotvt = kOffRotVT;
   H->off_rotkt = kOffRotKT;
   H->off_rows = kOffRows;
+  H->off_order = layout_order_offset(n_rows);
+  H->off_rowrot = layout_rowrot_offset(n_rows);
   H->total_bytes = total;
 
   const Codebooks& cb = codebooks();
@@ -457,6 +460,38 @@ int blockgtq_layout_init(const bgtq_config* cfg, const uint8_t* h_k_bits, const 
       M.word_first[w] = first;
     }
   }
+  // per-row rotation blocks and the decode dispatch orders
+  const float* rotkt_all = reinterpret_cast<const float*>(blob.data() + kOffRotKT);
+  std::vector<double> cost(n_rows);
+  for (int r = 0; r < n_rows; ++r) {
+    const RowMeta& M = rows[r];
+    float* dst = reinterpret_cast<float*>(blob.data() + layout_rowrot_offset(n_rows)) +
+                 static_cast<size_t>(r) * kRowRotFloats;
+    // decode work estimate of one 64-row tile: fixed part, per-group set-up,
+    // per-step cost by code width (relative units; only the order matters)
+    static const double kStep[9] = {0, 5.5, 3.75, 9.25, 7.75, 20, 20, 20, 20};
+    double c = 180.0;
+    for (int g = 0; g < M.n_groups; ++g) {
+      const int dg = M.g_dim[g];
+      std::memcpy(dst, rotkt_all + rotk_index(dg), sizeof(float) * dg * dg);
+      dst += dg * dg;
+      c += 15.0 + kStep[M.g_bits[g]] * ((dg + 3) / 4);
+    }
+    cost[r] = c;
+  }
+  int32_t* order_all = reinterpret_cast<int32_t*>(blob.data() + layout_order_offset(n_rows));
+  int32_t* order_layer = order_all + n_rows;
+  const auto by_cost = [&](int a, int b) { return cost[a] > cost[b] || (cost[a] == cost[b] && a < b); };
+  std::vector<int> idx(n_rows);
+  for (int r = 0; r < n_rows; ++r) idx[r] = r;
+  std::sort(idx.begin(), idx.end(), by_cost);
+  for (int r = 0; r < n_rows; ++r) order_all[r] = idx[r];
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    std::vector<int> hs(cfg->n_kv_heads);
+    for (int h = 0; h < cfg->n_kv_heads; ++h) hs[h] = l * cfg->n_kv_heads + h;
+    std::sort(hs.begin(), hs.end(), by_cost);
+    for (int h = 0; h < cfg->n_kv_heads; ++h) order_layer[l * cfg->n_kv_heads + h] = hs[h] - l * cfg->n_kv_heads;
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(d_layout, blob.data(), total, hipMemcpyHostToDevice, s);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(layout)");
@@ -490,6 +525,7 @@ static int check_decode_args(const bgtq_config* cfg, int32_t layer, const void* 
                              DecodeWs* ws, Kernel kern) {
   if (int e = check_cfg(cfg)) return e;
   if (!d_q || !d_ctx_len || !d_out || !d_ws) return fail(BGTQ_EINVAL, "NULL pointer");
+  if (reinterpret_cast<uintptr_t>(d_q) % 4 != 0) return fail(BGTQ_EINVAL, "q must be 4-byte aligned");
   if (layer < -1 || layer >= cfg->n_layers) return fail(BGTQ_EINVAL, "layer %d out of range", layer);
   if (max_ctx < 0 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [0, capacity]", max_ctx);
   if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);

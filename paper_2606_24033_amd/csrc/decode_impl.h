@@ -495,9 +495,25 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bq = lane >> 2, jq = lane & 3;
-  const int split = blockIdx.x, kvh = blockIdx.y, lz = blockIdx.z;
-  const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
-  const int seq = lz % d.batch;
+  // One-dimensional grid of (unit, split) items, units in the layout's
+  // dispatch order (most expensive rows first, so that the second round of
+  // workgroups fills in behind the long first ones); the splits of a unit
+  // are adjacent.
+  const int item = static_cast<int>(__builtin_amdgcn_workgroup_id_x());
+  const int split = item % n_splits, rest = item / n_splits;
+  const int seq = rest % d.batch, rank = rest / d.batch;
+  const int n_rows = d.n_layers * d.n_kv;
+  const int32_t* order = reinterpret_cast<const int32_t*>(blob + layout_order_offset(n_rows));
+  int layer, kvh;
+  if (d.layer >= 0) {
+    layer = d.layer;
+    kvh = order[n_rows + d.layer * d.n_kv + rank];
+  } else {
+    const int row = order[rank];
+    layer = row / d.n_kv;
+    kvh = row - layer * d.n_kv;
+  }
+  const int lz = d.layer >= 0 ? seq : layer * d.batch + seq;
   const int G = d.group, hqn = d.n_kv * G;
   const int cap = d.capacity, kw = d.k_words;
   const RowMeta* M = reinterpret_cast<const RowMeta*>(blob + kOffRows) + (layer * d.n_kv + kvh);
@@ -518,53 +534,60 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   }
   // ---- the Q-side rotation (Sec. 4): qr[h][p] = (Pi_g q_g)_j / sqrt(d_g d_h)
   // at stream position p = g_pos[g] + j.  Staged in LDS before the tables
-  // are built: qg[h][p] = q_h[dim(p)] (the queries gathered into stream
-  // order), qr, every group's rotation (transposed, one block after the
-  // other: sum_g d_g^2 <= 128^2 floats) and the codebooks.  All global reads
-  // of the set-up are issued together, before the first one is used.
-  static_assert(2 * 8 * kHeadDim * 4 + kHeadDim * kHeadDim * 4 <= kQimg + kQimgBytes, "rotation staging");
-  static_assert(2 * 8 * kHeadDim * 4 <= kQimg, "qr must survive the query image build");
+  // are built: the queries as given (qn), the row's group rotations (rs: the
+  // blocks Pi_dg transposed, one after the other, at the row's fixed slot in
+  // the layout), the stream-position -> dim table and the codebooks.  Every
+  // global read of the set-up is issued in one round (none depends on another
+  // read's value), then the queries are gathered into stream order (qg) and
+  // rotated (qr).
+  static_assert((2 * 8 * kHeadDim + kRowRotFloats + 8 * kHeadDim) * 4 + kHeadDim <= kQimg,
+                "set-up staging must stay below the query image");
   static_assert(8 * kHeadDim <= kThreads, "one query coordinate per thread");
-  constexpr int kRotPerThread = kHeadDim * kHeadDim / kThreads;
-  float* qg = reinterpret_cast<float*>(smem);      // [G][128]
-  float* qr = qg + 8 * kHeadDim;                   // [G][128]
-  float* rs = qr + 8 * kHeadDim;                   // staged rotations
+  float* qg = reinterpret_cast<float*>(smem);      // [G][128] queries in stream order
+  float* qr = qg + 8 * kHeadDim;                   // [G][128] rotated
+  float* rs = qr + 8 * kHeadDim;                   // the row's rotations, <= 128^2 floats
+  float* qn = rs + kRowRotFloats;                  // [G][128] queries as given
+  uint32_t* dimw = reinterpret_cast<uint32_t*>(qn + 8 * kHeadDim);  // RowMeta::dim
   uint16_t* cbs = reinterpret_cast<uint16_t*>(smem + kCbStage);
   // per-group rotation blocks: staged offset, size, first stream position
+  // (whole arrays read, entries past n_g replaced: no load waits on n_g)
   int roff[kMaxGroups], rdim[kMaxGroups], rpos[kMaxGroups];
   int rtot = 0;
 #pragma unroll
   for (int g = 0; g < kMaxGroups; ++g) {
-    rdim[g] = g < ng ? M->g_dim[g] : 0;
-    rpos[g] = g < ng ? M->g_pos[g] : kHeadDim;
+    const int a = M->g_dim[g], b = M->g_pos[g];
+    rdim[g] = g < ng ? a : 0;
+    rpos[g] = g < ng ? b : kHeadDim;
     roff[g] = rtot;
     rtot += rdim[g] * rdim[g];
   }
   {
-    const float* rotkt = reinterpret_cast<const float*>(blob + kOffRotKT);
-    const size_t qoff = (static_cast<size_t>(lz) * hqn + kvh * G) * kHeadDim;
-    const bool has_q = tid < G * kHeadDim;
-    const float qv = has_q ? ld_q(q, qoff + (tid >> 7) * kHeadDim + M->dim[tid & 127], d.in_dtype) : 0.f;
-    const uint32_t cv = tid < kCodebookEntries ? c16[tid] : 0u;
-    float rv[kRotPerThread];
+    constexpr int kRotFirst = kRowRotFloats / 2 / kThreads;  // per thread, always read
+    const float* rowrot = reinterpret_cast<const float*>(blob + layout_rowrot_offset(d.n_layers * d.n_kv)) +
+                          static_cast<size_t>(layer * d.n_kv + kvh) * kRowRotFloats;
+    // the query element of thread tid (clamped: in bounds, surplus unused),
+    // read as the aligned 32-bit word that holds it
+    const size_t qi = (static_cast<size_t>(lz) * hqn + kvh * G) * kHeadDim + min(tid, G * kHeadDim - 1);
+    const bool bf = d.in_dtype == 1;
+    const uint32_t qw = *reinterpret_cast<const uint32_t*>(static_cast<const uint8_t*>(q) +
+                                                           (bf ? (qi * 2) & ~static_cast<size_t>(3) : qi * 4));
+    const uint32_t mw = reinterpret_cast<const uint32_t*>(M->dim)[tid & 31];
+    const uint32_t cv = c16[min(tid, kCodebookEntries - 1)];
+    float rv[kRotFirst];
 #pragma unroll
-    for (int u = 0; u < kRotPerThread; ++u) {
-      const int i = tid + u * kThreads;
-      rv[u] = 0.f;
-      if (u * kThreads < rtot && i < rtot) {
-        int src = rotk_index(rdim[0]) + i;  // element i of the staged blocks in the source layout
-#pragma unroll
-        for (int g = 1; g < kMaxGroups; ++g)
-          if (g < ng && i >= roff[g]) src = rotk_index(rdim[g]) + (i - roff[g]);
-        rv[u] = rotkt[src];
-      }
-    }
-    if (has_q) qg[tid] = qv;
+    for (int u = 0; u < kRotFirst; ++u) rv[u] = rowrot[tid + u * kThreads];
+    if (tid < G * kHeadDim) qn[tid] = __uint_as_float(bf ? ((qi & 1) ? qw & 0xFFFF0000u : qw << 16) : qw);
+    if (tid < 32) dimw[tid] = mw;
     if (tid < kCodebookEntries) cbs[tid] = static_cast<uint16_t>(cv);
 #pragma unroll
-    for (int u = 0; u < kRotPerThread; ++u)
-      if (u * kThreads < rtot && tid + u * kThreads < rtot) rs[tid + u * kThreads] = rv[u];
+    for (int u = 0; u < kRotFirst; ++u)
+      if (tid + u * kThreads < rtot) rs[tid + u * kThreads] = rv[u];
+    // rows whose blocks exceed half the slot (few, large groups)
+    for (int i = tid + kRotFirst * kThreads; i < rtot; i += kThreads) rs[i] = rowrot[i];
   }
+  __syncthreads();
+  if (tid < G * kHeadDim)
+    qg[tid] = qn[(tid >> 7) * kHeadDim + reinterpret_cast<const uint8_t*>(dimw)[tid & 127]];
   __syncthreads();
   if (tid < G * kHeadDim) {
     // one rotated coordinate per thread: p = stream position, g its group
@@ -580,37 +603,54 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     const int j = p - p0;
     const float* rt = rs + off;  // Pi_dg transposed: rt[k dg + j] = Pi[j][k]
     const float* qq = qg + h * kHeadDim + p0;
-    float a0 = 0.f, a1 = 0.f;
-    for (int k = 0; k < dg; k += 2) {  // d_g is even
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    int k = 0;
+    for (; k + 4 <= dg; k += 4) {
+      a0 = fmaf(rt[k * dg + j], qq[k], a0);
+      a1 = fmaf(rt[(k + 1) * dg + j], qq[k + 1], a1);
+      a2 = fmaf(rt[(k + 2) * dg + j], qq[k + 2], a2);
+      a3 = fmaf(rt[(k + 3) * dg + j], qq[k + 3], a3);
+    }
+    if (k < dg) {  // d_g is even: two terms left
       a0 = fmaf(rt[k * dg + j], qq[k], a0);
       a1 = fmaf(rt[(k + 1) * dg + j], qq[k + 1], a1);
     }
-    qr[tid] = (a0 + a1) / sqrtf(static_cast<float>(dg) * kHeadDim);
+    qr[tid] = ((a0 + a1) + (a2 + a3)) / sqrtf(static_cast<float>(dg) * kHeadDim);
   }
   __syncthreads();
   // ---- query image: slot s, lane 4b+i holds step 16(s - slot0_g) + b of
-  // group g, head i of each set, 4 coordinates, as fp16 hi and lo parts
+  // group g, head i of each set, 4 coordinates, as fp16 hi and lo parts.
+  // Slots are numbered group after group; one pass over all of them.
   {
-    for (int g = 0; g < ng; ++g) {
-      const uint32_t meta = lds32(smem, kGmeta + 4 * (M->g_bits[g] - 1));
-      const int nst = gm_steps(meta), slot0 = gm_slot(meta);
-      const int gpos = M->g_pos[g], gdim = M->g_dim[g];
-      const int nchunk = (nst + 15) / 16;
-      for (int i = tid; i < nchunk * NSET * 64 * 4; i += kThreads) {
-        const int k = i & 3, l = (i >> 2) & 63, set = (i >> 8) % NSET, ch = (i >> 8) / NSET;
-        const int step = 16 * ch + (l >> 2), qh = 4 * set + (l & 3), coord = 4 * step + k;
-        float v = 0.f;
-        if (step < nst && coord < gdim && qh < G) v = qr[qh * kHeadDim + gpos + coord];
-        const _Float16 hi = static_cast<_Float16>(v);
-        const _Float16 lo = static_cast<_Float16>(v - static_cast<float>(hi));
-        uint8_t* dst = smem + kQimg + ((((slot0 + ch) * 2 + set) * 2) * 64 + l) * 8 + k * 2;
-        *reinterpret_cast<_Float16*>(dst) = hi;
-        *reinterpret_cast<_Float16*>(dst + 64 * 8) = lo;
-      }
+    int sl0[kMaxGroups], nslots = 0;
+#pragma unroll
+    for (int g = 0; g < kMaxGroups; ++g) {
+      sl0[g] = nslots;
+      nslots += ((rdim[g] + 3) / 4 + 15) / 16;
+    }
+    for (int i = tid; i < nslots * NSET * 64 * 4; i += kThreads) {
+      const int k = i & 3, l = (i >> 2) & 63, set = (i >> 8) % NSET, slot = (i >> 8) / NSET;
+      int gd = rdim[0], gp = rpos[0], s0 = sl0[0];
+#pragma unroll
+      for (int g = 1; g < kMaxGroups; ++g)
+        if (g < ng && slot >= sl0[g]) {
+          gd = rdim[g];
+          gp = rpos[g];
+          s0 = sl0[g];
+        }
+      const int step = 16 * (slot - s0) + (l >> 2), qh = 4 * set + (l & 3), coord = 4 * step + k;
+      float v = 0.f;
+      if (coord < gd && qh < G) v = qr[qh * kHeadDim + gp + coord];
+      const _Float16 hi = static_cast<_Float16>(v);
+      const _Float16 lo = static_cast<_Float16>(v - static_cast<float>(hi));
+      uint8_t* dst = smem + kQimg + (((slot * 2 + set) * 2) * 64 + l) * 8 + k * 2;
+      *reinterpret_cast<_Float16*>(dst) = hi;
+      *reinterpret_cast<_Float16*>(dst + 64 * 8) = lo;
     }
   }
   __syncthreads();
   // ---- lookup tables
+#pragma unroll
   for (int i = tid; i < 16 * 16; i += kThreads) {
     const int e = i >> 4;
     const uint16_t* cb = cbs + cb_index(1);
@@ -618,6 +658,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
         make_uint2(cb[e & 1] | (static_cast<uint32_t>(cb[(e >> 1) & 1]) << 16),
                    cb[(e >> 2) & 1] | (static_cast<uint32_t>(cb[(e >> 3) & 1]) << 16));
   }
+#pragma unroll
   for (int i = tid; i < 256 * 32; i += kThreads) {
     const int e = i >> 5;
     const uint16_t* cb = cbs + cb_index(2);
@@ -625,18 +666,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
         make_uint2(cb[e & 3] | (static_cast<uint32_t>(cb[(e >> 2) & 3]) << 16),
                    cb[(e >> 4) & 3] | (static_cast<uint32_t>(cb[(e >> 6) & 3]) << 16));
   }
+#pragma unroll
   for (int i = tid; i < 64 * 32; i += kThreads) {
     const int e = i >> 5;
     const uint16_t* cb = cbs + cb_index(3);
     *reinterpret_cast<uint32_t*>(smem + kLut3 + i * 4) = cb[e & 7] | (static_cast<uint32_t>(cb[(e >> 3) & 7]) << 16);
   }
+#pragma unroll
   for (int i = tid; i < 256 * 8; i += kThreads) {
     const int e = i >> 3;
     const uint16_t* cb = cbs + cb_index(4);
     *reinterpret_cast<uint32_t*>(smem + kLut4 + i * 4) = cb[e & 15] | (static_cast<uint32_t>(cb[e >> 4]) << 16);
   }
+#pragma unroll
   for (int i = tid; i < 32 * 32; i += kThreads)
     *reinterpret_cast<uint32_t*>(smem + kLut5 + i * 4) = cbs[cb_index(5) + (i >> 5)];
+#pragma unroll
   for (int i = tid; i < 64 + 128 + 256; i += kThreads) {
     const int b = i < 64 ? 6 : (i < 192 ? 7 : 8);
     const int k = i < 64 ? i : (i < 192 ? i - 64 : i - 192);
@@ -860,7 +905,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
 template <int BV>
 hipError_t launch_split_bv_impl(const Dims& d, const void* layout, const void* q, const int32_t* ctx_len,
                                 const CachePtrs& c, float* out, const DecodeWs& ws, hipStream_t s) {
-  dim3 grid(ws.n_splits, d.n_kv, d.batch * d.n_lc);
+  dim3 grid(ws.n_splits * d.n_kv * d.batch * d.n_lc);
   const uint8_t* blob = static_cast<const uint8_t*>(layout);
   const auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, d, blob, q, ctx_len, c, out, ws.counters, ws.part,

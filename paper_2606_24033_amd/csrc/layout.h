@@ -71,7 +71,9 @@ struct Header {
   uint64_t off_rotkt;    // float  [kRotKFloats] each Pi_d transposed, at rotk_index(d)
   uint64_t off_rows;     // RowMeta [n_rows]
   uint64_t total_bytes;
-  uint64_t pad1[5];
+  uint64_t off_order;    // int32 [2][n_rows]  row dispatch orders (see layout_order_offset)
+  uint64_t off_rowrot;   // float [n_rows][kRowRotFloats] per-row group rotations
+  uint64_t pad1[3];
 };
 static_assert(sizeof(Header) == 128, "Header size");
 
@@ -83,8 +85,22 @@ constexpr uint64_t kOffRotV = align256(kOffThr + 4 * kThresholdEntries);
 constexpr uint64_t kOffRotVT = align256(kOffRotV + 4 * kHeadDim * kHeadDim);
 constexpr uint64_t kOffRotKT = align256(kOffRotVT + 4 * kHeadDim * kHeadDim);
 constexpr uint64_t kOffRows = align256(kOffRotKT + 4ull * kRotKFloats);
+// After the row metadata:
+//  * two int32 [n_rows] dispatch orders of the rows, most expensive decode
+//    first (an estimate from the group widths): over all rows (entries are
+//    row indices), then per layer (entries are KV-head indices);
+//  * per row, its groups' rotations Pi_dg (transposed, as at rotk_index) one
+//    after the other, at a fixed stride of kRowRotFloats floats, so that a
+//    kernel can address them from the row index alone.
+constexpr int kRowRotFloats = kHeadDim * kHeadDim;
+__host__ __device__ constexpr uint64_t layout_order_offset(int n_rows) {
+  return align256(kOffRows + sizeof(RowMeta) * static_cast<uint64_t>(n_rows));
+}
+__host__ __device__ constexpr uint64_t layout_rowrot_offset(int n_rows) {
+  return align256(layout_order_offset(n_rows) + 8ull * static_cast<uint64_t>(n_rows));
+}
 __host__ __device__ constexpr uint64_t layout_total_bytes(int n_rows) {
-  return kOffRows + sizeof(RowMeta) * static_cast<uint64_t>(n_rows);
+  return layout_rowrot_offset(n_rows) + 4ull * kRowRotFloats * static_cast<uint64_t>(n_rows);
 }
 
 }  // namespace bgtq
