@@ -55,6 +55,9 @@ constexpr int kWaves = 16;  // one workgroup per CU: 160 KB of LDS for the table
 constexpr int kThreads = kWaves * 64;
 constexpr int kMaxSlots = 10;  // 16-step query slots of one key row: sum_g ceil(steps_g / 16)
 constexpr float kNegInf = -__builtin_huge_valf();
+constexpr float kLog2e = 1.4426950408889634f;
+// 2^x (the hardware exponential; arguments here are <= 0)
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // LDS map (bytes).  The b = 2 table has 32 replicas at a 256-byte entry
 // stride: the lanes of a half-wave read 32 distinct banks, and the address is
@@ -615,7 +618,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
       a0 = fmaf(rt[k * dg + j], qq[k], a0);
       a1 = fmaf(rt[(k + 1) * dg + j], qq[k + 1], a1);
     }
-    qr[tid] = ((a0 + a1) + (a2 + a3)) / sqrtf(static_cast<float>(dg) * kHeadDim);
+    // log2(e) folded in: logits come out in base-2 units for exp2
+    qr[tid] = ((a0 + a1) + (a2 + a3)) * (kLog2e / sqrtf(static_cast<float>(dg) * kHeadDim));
   }
   __syncthreads();
   // ---- query image: slot s, lane 4b+i holds step 16(s - slot0_g) + b of
@@ -749,39 +753,50 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     qk_all<NSET, KWB>(std::make_integer_sequence<int, 8>{}, smem, rw, knp, gmb, rep, lane, L);
 
     // ---------------- online softmax (lane 4b+i: head i, tokens 4b..4b+3)
-    const bool tok_in = tk < t_end;
-    const float vn4[4] = {h2f(vn.x & 0xFFFFu) * vscale, h2f(vn.x >> 16) * vscale,
-                          h2f(vn.y & 0xFFFFu) * vscale, h2f(vn.y >> 16) * vscale};
+    // Logits are in base-2 units (log2 e is folded into the query).  Only a
+    // tile that reaches past the split end masks anything: its scores past
+    // the end become -inf and their value radii 0.
+    const bool full = t0 + 64 <= t_end;
+    float vn4[4] = {h2f(vn.x & 0xFFFFu) * vscale, h2f(vn.x >> 16) * vscale, h2f(vn.y & 0xFFFFu) * vscale,
+                    h2f(vn.y >> 16) * vscale};
+    if (!full) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (t0 + 4 * bq + r >= t_end) vn4[r] = 0.f;
+    }
     half4_t pp[NSET];
 #pragma unroll
     for (int s = 0; s < NSET; ++s) {
       float4_t x = L[s];
-      if (!tok_in) x = float4_t{kNegInf, kNegInf, kNegInf, kNegInf};
+      if (!full && tk >= t_end) x = float4_t{kNegInf, kNegInf, kNegInf, kNegInf};
       quad_transpose(x, lane);
       float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
       mx = xmax16(mx);
       const float mn = fmaxf(m_run[s], mx);
-      const float corr = m_run[s] == kNegInf ? 0.f : __expf(m_run[s] - mn);
+      const float corr = m_run[s] == kNegInf ? 0.f : exp2_hw(m_run[s] - mn);
       float ps = 0.f;
       uint32_t ph[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = __expf(x[r] - mn);
+        const float p = exp2_hw(x[r] - mn);
         ps += p;
-        const float pv = (t0 + 4 * bq + r < t_end) ? p * vn4[r] : 0.f;
-        ph[r] = __half_as_ushort(__float2half_rn(pv));
+        ph[r] = __half_as_ushort(__float2half_rn(p * vn4[r]));
       }
       pp[s] = as_half4(ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16));
       l_run[s] = l_run[s] * corr + ps;  // this lane's tokens only; reduced after the loop
-      m_run[s] = mn;
-      const float c0 = qperm<0x00>(corr), c1 = qperm<0x55>(corr), c2 = qperm<0xAA>(corr), c3 = qperm<0xFF>(corr);
+      // the accumulators are rescaled only when some running maximum moved
+      // (otherwise corr is exactly 1); the test is one wave-wide vote
+      if (__builtin_amdgcn_ballot_w64(mn != m_run[s]) != 0) {
+        const float c0 = qperm<0x00>(corr), c1 = qperm<0x55>(corr), c2 = qperm<0xAA>(corr), c3 = qperm<0xFF>(corr);
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        O[s][h][0] *= c0;
-        O[s][h][1] *= c1;
-        O[s][h][2] *= c2;
-        O[s][h][3] *= c3;
+        for (int h = 0; h < 2; ++h) {
+          O[s][h][0] *= c0;
+          O[s][h][1] *= c1;
+          O[s][h][2] *= c2;
+          O[s][h][3] *= c3;
+        }
       }
+      m_run[s] = mn;
     }
 
     // ---------------- PV: 16 steps of 4 tokens (lane = dim)
@@ -818,7 +833,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
       for (int w = 0; w < kWaves; ++w) {
         const float mw = fm[w * 8 + qh];
         if (mw == kNegInf) continue;
-        const float e = __expf(mw - mx);
+        const float e = exp2_hw(mw - mx);
         l = fmaf(fl[w * 8 + qh], e, l);
         a = fmaf(fo[(w * 8 + qh) * kHeadDim + dd], e, a);
       }
@@ -874,13 +889,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
 #pragma unroll
         for (int u = 0; u < 8; ++u) mc = fmaxf(mc, ms[u]);
         if (mc == kNegInf) continue;
-        const float r = mx == kNegInf ? 0.f : __expf(mx - mc);
+        const float r = mx == kNegInf ? 0.f : exp2_hw(mx - mc);
         l *= r;
         a *= r;
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           if (ms[u] == kNegInf) continue;
-          const float e = __expf(ms[u] - mc);
+          const float e = exp2_hw(ms[u] - mc);
           l = fmaf(ls[u], e, l);
           a = fmaf(as[u], e, a);
         }
