@@ -70,7 +70,8 @@ constexpr int kLut3 = kLut1 + 16 * 16 * 8;      // b=3: 64 (2 codes) x 32 x 4
 constexpr int kLut4 = kLut3 + 64 * 32 * 4;      // b=4: 256 (2 codes) x 8 x 4
 constexpr int kLut5 = kLut4 + 256 * 8 * 4;      // b=5: 32 (1 code, low half) x 32 x 4
 constexpr int kLutF = kLut5 + 32 * 32 * 4;      // b=6,7,8: plain fp16 tables at +0, +128, +384
-constexpr int kQimg = kLutF + 1024;             // [slot][set][hi,lo][lane] x 8 B
+constexpr int kLut1B = kLutF + 1024;            // b=1 keys: 256 entries (8 codes) x 8 replicas x 16 B
+constexpr int kQimg = kLut1B + 256 * 8 * 16;    // [slot][set][hi,lo][lane] x 8 B
 constexpr int kQimgBytes = kMaxSlots * 2 * 2 * 64 * 8;
 constexpr int kGmeta = kQimg + kQimgBytes;      // [b - 1] packed group metadata
 constexpr int kCbStage = kGmeta + 64;           // fp16 codebooks, staged for the table build
@@ -205,6 +206,7 @@ struct LaneRep {
   uint32_t r32;  // (lane & 31) * 4
   uint32_t r8;   // (lane & 7) * 4
   uint32_t r2;   // (lane & 31) * 8: replica offset in the b = 2 table
+  uint32_t r1b;  // (lane & 7) * 16: replica offset in the 8-code b = 1 table
 };
 
 // Byte K of w (a compile-time byte) as the entry index of the b = 2 table:
@@ -274,7 +276,25 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
                                           const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
                                           float4_t (&acc)[NSET]) {
   constexpr int k = 4 * W;
-  if constexpr (B <= 4) {
+  if constexpr (B == 1) {
+    // one 16-byte lookup per code byte: the operands of two steps
+    constexpr int by = k / 2;  // byte of step k
+    const uint4 u01 = *reinterpret_cast<const uint4*>(
+        smem + kLut1B + ((__builtin_amdgcn_ubfe(aw[by / 4], 8 * (by % 4), 8) << 7) | rep.r1b));
+    const uint4 u23 = *reinterpret_cast<const uint4*>(
+        smem + kLut1B + ((__builtin_amdgcn_ubfe(aw[(by + 1) / 4], 8 * ((by + 1) % 4), 8) << 7) | rep.r1b));
+    half4_t kv0 = as_half4(u01.x, u01.y), kv1 = as_half4(u01.z, u01.w);
+    half4_t kv2 = as_half4(u23.x, u23.y), kv3 = as_half4(u23.z, u23.w);
+    asm volatile("" : "+v"(kv0), "+v"(kv1), "+v"(kv2), "+v"(kv3));
+    qk_mac<NSET, K0 + k>(kv0, qh, ql, acc);
+    if (mm > k + 1) {
+      qk_mac<NSET, K0 + k + 1>(kv1, qh, ql, acc);
+      if (mm > k + 2) {
+        qk_mac<NSET, K0 + k + 2>(kv2, qh, ql, acc);
+        if (mm > k + 3) qk_mac<NSET, K0 + k + 3>(kv3, qh, ql, acc);
+      }
+    }
+  } else if constexpr (B <= 4) {
     half4_t kv0 = decode4<B, 4 * B * (k + 0)>(smem, aw, rep);
     half4_t kv1 = decode4<B, 4 * B * (k + 1)>(smem, aw, rep);
     half4_t kv2 = decode4<B, 4 * B * (k + 2)>(smem, aw, rep);
@@ -663,6 +683,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
                    cb[(e >> 2) & 1] | (static_cast<uint32_t>(cb[(e >> 3) & 1]) << 16));
   }
 #pragma unroll
+  for (int i = tid; i < 256 * 8; i += kThreads) {
+    const int e = i >> 3;  // code byte: bit c is the code of coordinate c
+    const uint16_t* cb = cbs + cb_index(1);
+    const auto pair = [&](int c) { return cb[(e >> c) & 1] | (static_cast<uint32_t>(cb[(e >> (c + 1)) & 1]) << 16); };
+    *reinterpret_cast<uint4*>(smem + kLut1B + i * 16) = make_uint4(pair(0), pair(2), pair(4), pair(6));
+  }
+#pragma unroll
   for (int i = tid; i < 256 * 32; i += kThreads) {
     const int e = i >> 5;
     const uint16_t* cb = cbs + cb_index(2);
@@ -697,7 +724,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
 #pragma unroll
   for (int b = 0; b < 8; ++b) gmb[b] = __builtin_amdgcn_readfirstlane(lds32(smem, kGmeta + 4 * b));
   const LaneRep rep{static_cast<uint32_t>(lane & 15) * 8u, static_cast<uint32_t>(lane & 31) * 4u,
-                    static_cast<uint32_t>(lane & 7) * 4u, static_cast<uint32_t>(lane & 31) * 8u};
+                    static_cast<uint32_t>(lane & 7) * 4u, static_cast<uint32_t>(lane & 31) * 8u,
+                    static_cast<uint32_t>(lane & 7) * 16u};
 
   const int ctx = min(ctx_len[seq], cap);
   const int t_begin = split * split_len;
