@@ -36,10 +36,12 @@
 // 64-bit entry of four fp16 centroids), 2 codes for b = 3, 4, 1 code above.
 // The rotated query is split into fp16 hi and lo parts (both multiplied,
 // accumulated in fp32): fp16 alone leaves ~2^-12 relative error per term.
+// 1-bit groups take the hi part only.
 #pragma once
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
 #include <utility>
 
 #include "kernels.h"
@@ -254,14 +256,18 @@ constexpr int kRowPad = 4;  // zero words after a key row: a sub-chunk reads wor
 template <int B>
 constexpr int qk_nw() { return (qk_ch<B>() * 4 * B + 31) / 32; }  // words per sub-chunk
 
-// One MFMA pair (hi and lo query parts) of query block K.
-template <int NSET, int K>
+// One MFMA pair (hi and lo query parts) of query block K; LO = false leaves
+// out the lo part (1-bit groups: their terms are the smallest, see below).
+template <int NSET, int K, bool LO = true, bool Z = false>
 __device__ __forceinline__ void qk_mac(const half4_t& kv, const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
                                        float4_t (&acc)[NSET]) {
 #pragma unroll
   for (int s = 0; s < NSET; ++s) {
-    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(qh[s], kv, acc[s], 4, K, 0);
-    acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(ql[s], kv, acc[s], 4, K, 0);
+    if constexpr (Z)  // the group's first product starts its accumulator
+      acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(qh[s], kv, float4_t{0.f, 0.f, 0.f, 0.f}, 4, K, 0);
+    else
+      acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(qh[s], kv, acc[s], 4, K, 0);
+    if constexpr (LO) acc[s] = __builtin_amdgcn_mfma_f32_4x4x4f16(ql[s], kv, acc[s], 4, K, 0);
   }
 }
 
@@ -271,13 +277,16 @@ __device__ __forceinline__ void qk_mac(const half4_t& kv, const half4_t (&qh)[NS
 // the row or its zero padding: a valid table index, whose MFMA is skipped),
 // so the decoded operands need no merge copies; wider codes take four
 // lookups a step and are decoded only when the step exists.
-template <int B, int NSET, int K0, int W, int N>
+template <int B, int NSET, int K0, int W, int N, bool Z = false>
 __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&aw)[N], int mm, const LaneRep& rep,
                                           const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
                                           float4_t (&acc)[NSET]) {
   constexpr int k = 4 * W;
   if constexpr (B == 1) {
-    // one 16-byte lookup per code byte: the operands of two steps
+    // one 16-byte lookup per code byte: the operands of two steps.  Only the
+    // hi query part: 1-bit blocks are the ones with the least energy, and
+    // leaving out their lo products moves the attention output by ~1e-4
+    // (relative), against ~1e-3 for leaving out every lo product.
     constexpr int by = k / 2;  // byte of step k
     const uint4 u01 = *reinterpret_cast<const uint4*>(
         smem + kLut1B + ((__builtin_amdgcn_ubfe(aw[by / 4], 8 * (by % 4), 8) << 7) | rep.r1b));
@@ -286,12 +295,12 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
     half4_t kv0 = as_half4(u01.x, u01.y), kv1 = as_half4(u01.z, u01.w);
     half4_t kv2 = as_half4(u23.x, u23.y), kv3 = as_half4(u23.z, u23.w);
     asm volatile("" : "+v"(kv0), "+v"(kv1), "+v"(kv2), "+v"(kv3));
-    qk_mac<NSET, K0 + k>(kv0, qh, ql, acc);
+    qk_mac<NSET, K0 + k, false, Z>(kv0, qh, ql, acc);
     if (mm > k + 1) {
-      qk_mac<NSET, K0 + k + 1>(kv1, qh, ql, acc);
+      qk_mac<NSET, K0 + k + 1, false>(kv1, qh, ql, acc);
       if (mm > k + 2) {
-        qk_mac<NSET, K0 + k + 2>(kv2, qh, ql, acc);
-        if (mm > k + 3) qk_mac<NSET, K0 + k + 3>(kv3, qh, ql, acc);
+        qk_mac<NSET, K0 + k + 2, false>(kv2, qh, ql, acc);
+        if (mm > k + 3) qk_mac<NSET, K0 + k + 3, false>(kv3, qh, ql, acc);
       }
     }
   } else if constexpr (B <= 4) {
@@ -303,7 +312,7 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
     // trip per window): without this the compiler sinks each lookup into
     // the branch that uses it and serialises them
     asm volatile("" : "+v"(kv0), "+v"(kv1), "+v"(kv2), "+v"(kv3));
-    qk_mac<NSET, K0 + k>(kv0, qh, ql, acc);
+    qk_mac<NSET, K0 + k, true, Z>(kv0, qh, ql, acc);
     if (mm > k + 1) {
       qk_mac<NSET, K0 + k + 1>(kv1, qh, ql, acc);
       if (mm > k + 2) {
@@ -312,7 +321,7 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
       }
     }
   } else {
-    qk_mac<NSET, K0 + k>(decode4<B, 4 * B * k>(smem, aw, rep), qh, ql, acc);
+    qk_mac<NSET, K0 + k, true, Z>(decode4<B, 4 * B * k>(smem, aw, rep), qh, ql, acc);
     if (mm > k + 1) {
       qk_mac<NSET, K0 + k + 1>(decode4<B, 4 * B * (k + 1)>(smem, aw, rep), qh, ql, acc);
       if (mm > k + 2) {
@@ -325,12 +334,13 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
 
 // Sub-chunk SC of a 16-step slot: realign its bits (stream bit ob onwards)
 // to bit 0 of aw, then run its min(CH, ms - SC CH) steps.
-template <int B, int NSET, int KWB, int SC>
+template <int B, int NSET, int KWB, bool Z, int SC>
 __device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t (&rw)[KWB + kRowPad], int ob, int ms,
                                              const LaneRep& rep, const half4_t (&qh)[NSET],
                                              const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
   constexpr int CH = qk_ch<B>(), NW = qk_nw<B>();
-  if (SC * CH < ms) {
+  // (with Z, sub-chunk 0 always exists: a group has at least one step)
+  if ((Z && SC == 0) || SC * CH < ms) {
     const int o = ob + SC * CH * 4 * B;
     const int w0 = o >> 5, sh = o & 31;
     uint32_t aw[NW + 1];
@@ -338,18 +348,18 @@ __device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t
     for (int i = 0; i < NW; ++i) aw[i] = __builtin_amdgcn_alignbit(rw[w0 + i + 1], rw[w0 + i], sh);
     aw[NW] = 0;
     const int mm = min(CH, ms - SC * CH);
-    qk_window<B, NSET, SC * CH, 0, NW + 1>(smem, aw, mm, rep, qh, ql, acc);
+    qk_window<B, NSET, SC * CH, 0, NW + 1, Z && SC == 0>(smem, aw, mm, rep, qh, ql, acc);
     if constexpr (CH == 8) {
       if (mm > 4) qk_window<B, NSET, SC * CH, 1, NW + 1>(smem, aw, mm, rep, qh, ql, acc);
     }
   }
 }
 
-template <int B, int NSET, int KWB, int... SC>
+template <int B, int NSET, int KWB, bool Z, int... SC>
 __device__ __forceinline__ void qk_slot(std::integer_sequence<int, SC...>, const uint8_t* smem,
                                         const uint32_t (&rw)[KWB + kRowPad], int ob, int ms, const LaneRep& rep,
                                         const half4_t (&qh)[NSET], const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
-  (qk_slot_part<B, NSET, KWB, SC>(smem, rw, ob, ms, rep, qh, ql, acc), ...);
+  (qk_slot_part<B, NSET, KWB, Z, SC>(smem, rw, ob, ms, rep, qh, ql, acc), ...);
 }
 
 // The group of width B (metadata gm, radius bits nrm16 of the lane's token):
@@ -359,9 +369,8 @@ __device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&r
                                          uint32_t nrm16, const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
   const int o = gm_off(gm), nst = gm_steps(gm), slot0 = gm_slot(gm);
   float4_t acc[NSET];
-#pragma unroll
-  for (int s = 0; s < NSET; ++s) acc[s] = float4_t{0.f, 0.f, 0.f, 0.f};
-  for (int c = 0; c * 16 < nst; ++c) {
+  // slot 0 is peeled: its first product writes the accumulator
+  const auto slot = [&](auto first, int c) {
     half4_t qh[NSET], ql[NSET];
 #pragma unroll
     for (int s = 0; s < NSET; ++s) {
@@ -370,9 +379,11 @@ __device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&r
       qh[s] = as_half4(uh.x, uh.y);
       ql[s] = as_half4(ul.x, ul.y);
     }
-    qk_slot<B, NSET, KWB>(std::make_integer_sequence<int, 16 / qk_ch<B>()>{}, smem, rw, o + 64 * B * c,
-                          min(16, nst - 16 * c), rep, qh, ql, acc);
-  }
+    qk_slot<B, NSET, KWB, decltype(first)::value>(std::make_integer_sequence<int, 16 / qk_ch<B>()>{}, smem, rw,
+                                                  o + 64 * B * c, min(16, nst - 16 * c), rep, qh, ql, acc);
+  };
+  slot(std::true_type{}, 0);
+  for (int c = 1; c * 16 < nst; ++c) slot(std::false_type{}, c);
   const float nrm = h2f(nrm16);
 #pragma unroll
   for (int s = 0; s < NSET; ++s)
