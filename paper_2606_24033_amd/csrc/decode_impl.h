@@ -527,7 +527,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     CachePtrs c, float* __restrict__ out, int32_t* __restrict__ counters, float* __restrict__ part, int n_splits,
     int split_len) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: tile addresses stay scalar
   const int bq = lane >> 2, jq = lane & 3;
   // One-dimensional grid of (unit, split) items, units in the layout's
   // dispatch order (most expensive rows first, so that the second round of
