@@ -433,6 +433,12 @@ int blockgtq_layout_init(const bgtq_config* cfg, const uint8_t* h_k_bits, const 
       }
     }
     M.n_groups = g;
+    for (int w = 0, slot = 0; w < g; ++w) {
+      const uint32_t nst = static_cast<uint32_t>(M.g_dim[w] + 3) / 4;
+      M.gm[M.g_bits[w] - 1] = (1u << 31) | static_cast<uint32_t>(M.bitoff[M.g_pos[w]]) | (nst << 10) |
+                              (static_cast<uint32_t>(slot) << 16) | (static_cast<uint32_t>(w) << 20);
+      slot += static_cast<int>((nst + 15) / 16);
+    }
     // decode steps: 4 coordinates of one group per step
     int ns = 0;
     for (int gg = 0; gg < g; ++gg) {

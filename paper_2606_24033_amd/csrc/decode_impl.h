@@ -75,7 +75,7 @@ constexpr int kLutF = kLut5 + 32 * 32 * 4;      // b=6,7,8: plain fp16 tables at
 constexpr int kLut1B = kLutF + 1024;            // b=1 keys: 256 entries (8 codes) x 8 replicas x 16 B
 constexpr int kQimg = kLut1B + 256 * 8 * 16;    // [slot][set][hi,lo][lane] x 8 B
 constexpr int kQimgBytes = kMaxSlots * 2 * 2 * 64 * 8;
-constexpr int kGmeta = kQimg + kQimgBytes;      // [b - 1] packed group metadata
+constexpr int kGmeta = kQimg + kQimgBytes;      // flag word of the split merge
 constexpr int kCbStage = kGmeta + 64;           // fp16 codebooks, staged for the table build
 constexpr int kLdsBytes = kCbStage + 2 * 512;
 static_assert(2 * kCodebookEntries <= 2 * 512, "codebook staging");
@@ -555,18 +555,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   const uint16_t* c16 = reinterpret_cast<const uint16_t*>(blob + kOffC16);
   const int ng = M->n_groups;
 
-  // ---- group metadata by width; each group's steps start a new query slot
-  if (tid == 0) {
-    uint32_t* gmw = reinterpret_cast<uint32_t*>(smem + kGmeta);
-    for (int b = 0; b < 8; ++b) gmw[b] = 0u;
-    uint32_t slot = 0;
-    for (int g = 0; g < ng; ++g) {
-      const uint32_t nst = (M->g_dim[g] + 3) / 4;
-      gmw[M->g_bits[g] - 1] = (1u << 31) | static_cast<uint32_t>(M->bitoff[M->g_pos[g]]) | (nst << 10) |
-                              (slot << 16) | (static_cast<uint32_t>(g) << 20);
-      slot += (nst + 15) / 16;
-    }
-  }
   // ---- the Q-side rotation (Sec. 4): qr[h][p] = (Pi_g q_g)_j / sqrt(d_g d_h)
   // at stream position p = g_pos[g] + j.  Staged in LDS before the tables
   // are built: the queries as given (qn), the row's group rotations (rs: the
@@ -733,8 +721,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   __syncthreads();
 
   uint32_t gmb[8];
-#pragma unroll
-  for (int b = 0; b < 8; ++b) gmb[b] = __builtin_amdgcn_readfirstlane(lds32(smem, kGmeta + 4 * b));
   const LaneRep rep{static_cast<uint32_t>(lane & 15) * 8u, static_cast<uint32_t>(lane & 31) * 4u,
                     static_cast<uint32_t>(lane & 7) * 4u, static_cast<uint32_t>(lane & 31) * 8u,
                     static_cast<uint32_t>(lane & 7) * 16u};
@@ -778,12 +764,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     if (t0 + stride < t_end) load_keys<KWB>(rw2, knp2, nslot, R, kw, t0 + stride, lane);
     const int tk = t0 + lane;
     {
-      // Re-read the width metadata every tile (through an opaque address):
-      // hoisted out of the loop, its derived scalars exhaust the SGPRs.
-      uint32_t goff = kGmeta;
-      asm volatile("" : "+v"(goff));
+      // Re-read the row's width table every tile (scalar loads through an
+      // opaque offset): hoisted out of the loop, its derived scalars exhaust
+      // the SGPRs.
+      uint32_t goff = 0;
+      asm volatile("" : "+s"(goff));
+      const uint32_t* gmt = reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(M->gm) + goff);
 #pragma unroll
-      for (int b = 0; b < 8; ++b) gmb[b] = __builtin_amdgcn_readfirstlane(lds32(smem, goff + 4 * b));
+      for (int b = 0; b < 8; ++b) gmb[b] = gmt[b];
     }
 
     // ---------------- QK, one same-rate group at a time (lane = token)

@@ -53,7 +53,12 @@ struct RowMeta {
   uint32_t step[kMaxSteps];
   int32_t n_steps;
   int32_t word_step[kMaxKWords + 1];  // steps starting in word w: [word_step[w], word_step[w+1])
-  int32_t pad[21];
+  // packed decode metadata by width b (entry b - 1; 0 = width absent): bit 31
+  // present, bits 0..9 first stream bit, 10..15 steps, 16..19 first query
+  // slot (16 steps per slot, slots numbered group after group), 20..22 the
+  // group ordinal
+  uint32_t gm[8];
+  int32_t pad[13];
 };
 static_assert(sizeof(RowMeta) == 1280, "RowMeta size");
 
