@@ -42,8 +42,8 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--ctx", type=int, default=131072)
     ap.add_argument("--n-splits", type=int, default=0)
     ap.add_argument("--no-fp16", action="store_true", help="skip the fp16 comparator")
