@@ -209,6 +209,7 @@ struct LaneRep {
   uint32_t r8;   // (lane & 7) * 4
   uint32_t r2;   // (lane & 31) * 8: replica offset in the b = 2 table
   uint32_t r1b;  // (lane & 7) * 16: replica offset in the 8-code b = 1 table
+  uint32_t qimg; // kQimg + lane * 8: this lane's entry in slot 0 of the query image
 };
 
 // Byte K of w (a compile-time byte) as the entry index of the b = 2 table:
@@ -374,7 +375,7 @@ __device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&r
     half4_t qh[NSET], ql[NSET];
 #pragma unroll
     for (int s = 0; s < NSET; ++s) {
-      const uint32_t base = kQimg + (((slot0 + c) * 2 + s) * 2 * 64 + lane) * 8;
+      const uint32_t base = rep.qimg + ((slot0 + c) * 2 + s) * 2 * 64 * 8;  // slot offset: one add
       const uint2 uh = lds64(smem, base), ul = lds64(smem, base + 64 * 8);
       qh[s] = as_half4(uh.x, uh.y);
       ql[s] = as_half4(ul.x, ul.y);
@@ -504,9 +505,8 @@ __device__ __forceinline__ void load_values(uint2& vn, uint32_t (&vw)[4][pv_word
 
 // Radius bits of group ordinal g (wave-uniform) from the packed halves.
 __device__ __forceinline__ uint32_t radius_bits(const uint32_t (&knp)[4], int g) {
-  const int i = g >> 1;
-  const uint32_t w = i == 0 ? knp[0] : (i == 1 ? knp[1] : (i == 2 ? knp[2] : knp[3]));
-  return (w >> (16 * (g & 1))) & 0xFFFFu;
+  // g is wave-uniform: one indexed register move, then the half
+  return knp[g >> 1] >> (16 * (g & 1));
 }
 
 // QK of one tile over every present width.
@@ -723,7 +723,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   uint32_t gmb[8];
   const LaneRep rep{static_cast<uint32_t>(lane & 15) * 8u, static_cast<uint32_t>(lane & 31) * 4u,
                     static_cast<uint32_t>(lane & 7) * 4u, static_cast<uint32_t>(lane & 31) * 8u,
-                    static_cast<uint32_t>(lane & 7) * 16u};
+                    static_cast<uint32_t>(lane & 7) * 16u, static_cast<uint32_t>(kQimg + lane * 8)};
 
   const int ctx = min(ctx_len[seq], cap);
   const int t_begin = split * split_len;
