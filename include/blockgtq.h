@@ -121,8 +121,7 @@ int blockgtq_cache_bytes(const bgtq_config* cfg, size_t* k_codes, size_t* k_norm
                          size_t* v_codes, size_t* v_norms);
 /* Workspace of one blockgtq_decode_attn (or _fp16) call: n_layers_in_call =
  * 1 for a single layer, cfg->n_layers for layer = -1.  n_splits as passed to
- * the call (0 = the heuristic for max_ctx, which differs between the two
- * entry points; the size returned covers either).  The workspace starts with one int32
+ * the call (0 = the heuristic for max_ctx).  The workspace starts with one int32
  * counter per (layer in call, sequence, KV head) that the kernel uses to find
  * the last split to finish: it must be zero-filled once before its first
  * use, and every completed call leaves it zero again.  Calls that share a
@@ -194,7 +193,8 @@ int blockgtq_decode_attn(const bgtq_config* cfg, const void* d_layout, int32_t l
  * baseline the packed path's speedup is reported against (the paper compares
  * with fp16 FlashAttention-2 decode, Sec. 6 deployment).
  * d_k16, d_v16: fp16 [n_layers][batch][n_kv_heads][capacity][head_dim].
- * Other arguments as blockgtq_decode_attn (no layout blob: no codes). */
+ * Other arguments as blockgtq_decode_attn (no layout blob: no codes, no
+ * rotations); the same MFMA products, softmax and split merge. */
 int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void* d_q,
                               const int32_t* d_ctx_len, int32_t max_ctx,
                               const void* d_k16, const void* d_v16, float* d_out,

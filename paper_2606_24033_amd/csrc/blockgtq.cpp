@@ -207,14 +207,11 @@ struct SplitPlan {
   int n_splits, split_len;
 };
 
-// Default split counts: the packed decode runs one 16-wave workgroup per CU at
+// Default split count: the decode kernels run one 16-wave workgroup per CU at
 // a time, two rounds (the second round's workgroups go to the CUs that finish
 // first, so the work evens out), each split at least 1024 rows (a 64-row tile
-// per wave); the fp16 comparator runs 4-wave workgroups and wants about eight
-// per CU, each split at least 256 rows.
-enum class Kernel { kPacked, kFp16 };
-
-SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested, Kernel k = Kernel::kPacked) {
+// per wave).
+SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested) {
   SplitPlan p;
   if (max_ctx <= 0) return {1, 64};
   const int max_splits = (max_ctx + kTile - 1) / kTile;
@@ -223,10 +220,8 @@ SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested
     n = std::min(requested, max_splits);
   } else {
     const long units = static_cast<long>(c->n_kv_heads) * c->batch * n_lc;
-    const long wgs = k == Kernel::kPacked ? 512 : 2048;
-    const int min_len = k == Kernel::kPacked ? 1024 : 256;
-    n = static_cast<int>((wgs + units - 1) / units);
-    n = std::max(1, std::min(n, (max_ctx + min_len - 1) / min_len));
+    n = static_cast<int>((512 + units - 1) / units);
+    n = std::max(1, std::min(n, (max_ctx + 1023) / 1024));
   }
   p.split_len = ((max_ctx + n - 1) / n + 63) / 64 * 64;
   p.n_splits = (max_ctx + p.split_len - 1) / p.split_len;
@@ -345,10 +340,7 @@ int blockgtq_workspace_bytes(const bgtq_config* cfg, int32_t n_layers_in_call, i
     return fail(BGTQ_EINVAL, "n_layers_in_call must be 1 or n_layers");
   if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);
   if (max_ctx < 0 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [0, capacity]", max_ctx);
-  // enough for either decode entry point
-  *bytes_out = std::max(ws_bytes_of(cfg, n_layers_in_call, plan_splits(cfg, n_layers_in_call, max_ctx, n_splits)),
-                        ws_bytes_of(cfg, n_layers_in_call,
-                                    plan_splits(cfg, n_layers_in_call, max_ctx, n_splits, Kernel::kFp16)));
+  *bytes_out = ws_bytes_of(cfg, n_layers_in_call, plan_splits(cfg, n_layers_in_call, max_ctx, n_splits));
   return ok();
 }
 
@@ -528,7 +520,7 @@ int blockgtq_quantize_append(const bgtq_config* cfg, const void* d_layout, int32
 
 static int check_decode_args(const bgtq_config* cfg, int32_t layer, const void* d_q, const int32_t* d_ctx_len,
                              int32_t max_ctx, float* d_out, void* d_ws, size_t ws_bytes, int32_t n_splits,
-                             DecodeWs* ws, Kernel kern) {
+                             DecodeWs* ws) {
   if (int e = check_cfg(cfg)) return e;
   if (!d_q || !d_ctx_len || !d_out || !d_ws) return fail(BGTQ_EINVAL, "NULL pointer");
   if (reinterpret_cast<uintptr_t>(d_q) % 4 != 0) return fail(BGTQ_EINVAL, "q must be 4-byte aligned");
@@ -536,7 +528,7 @@ static int check_decode_args(const bgtq_config* cfg, int32_t layer, const void* 
   if (max_ctx < 0 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [0, capacity]", max_ctx);
   if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);
   const int n_lc = layer < 0 ? cfg->n_layers : 1;
-  const SplitPlan p = plan_splits(cfg, n_lc, max_ctx, n_splits, kern);
+  const SplitPlan p = plan_splits(cfg, n_lc, max_ctx, n_splits);
   const size_t need = ws_bytes_of(cfg, n_lc, p);
   if (ws_bytes < need) return fail(BGTQ_EWORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
   ws->counters = static_cast<int32_t*>(d_ws);
@@ -550,8 +542,7 @@ int blockgtq_decode_attn(const bgtq_config* cfg, const void* d_layout, int32_t l
                          const int32_t* d_ctx_len, int32_t max_ctx, const bgtq_cache* cache, float* d_out,
                          void* d_workspace, size_t ws_bytes, int32_t n_splits, void* stream) {
   DecodeWs ws;
-  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws,
-                                Kernel::kPacked))
+  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws))
     return e;
   if (!d_layout || !cache || !cache->k_codes || !cache->k_norms || !cache->v_codes || !cache->v_norms)
     return fail(BGTQ_EINVAL, "NULL pointer");
@@ -567,8 +558,7 @@ int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void*
                               int32_t max_ctx, const void* d_k16, const void* d_v16, float* d_out,
                               void* d_workspace, size_t ws_bytes, int32_t n_splits, void* stream) {
   DecodeWs ws;
-  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws,
-                                Kernel::kFp16))
+  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws))
     return e;
   if (!d_k16 || !d_v16) return fail(BGTQ_EINVAL, "NULL pointer");
   hipError_t e = launch_decode_fp16(dims_of(cfg, layer), d_q, d_ctx_len, d_k16, d_v16, d_out, ws,

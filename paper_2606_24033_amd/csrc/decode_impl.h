@@ -520,6 +520,134 @@ __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const
    ...);
 }
 
+// ---------------------------------------------------------------- epilogue
+// Merge of the waves' (max, sum, accumulator) states in LDS, then (n_splits
+// > 1) of the splits of the unit in the workgroup that finishes it last
+// (exact log-sum-exp; it resets the unit's counter), then out = R^T o with R
+// the V rotation (rotv) or none.  The merge area of LDS starts at smem;
+// `last` is a flag word outside it.
+template <int NSET>
+__device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims& d, int G, int lz, int kvh,
+                                            int split, int tid, int lane, int wave, float (&m_run)[NSET],
+                                            float (&l_run)[NSET], const float4_t (&O)[NSET][2],
+                                            int32_t* __restrict__ counters, float* __restrict__ part, int n_splits,
+                                            const float* __restrict__ rotv, float* __restrict__ out) {
+  const int hqn = d.n_kv * G;
+  const int bq = lane >> 2, jq = lane & 3;
+#pragma unroll
+  for (int s = 0; s < NSET; ++s) l_run[s] = xsum16(l_run[s]);
+
+  // ---------------- merge the waves of the workgroup
+  __syncthreads();
+  float* fm = reinterpret_cast<float*>(smem);            // [wave][8] max
+  float* fl = fm + kWaves * 8;                           // [wave][8] sum
+  float* fo = fl + kWaves * 8;                           // [wave][8][128] accumulators
+#pragma unroll
+  for (int s = 0; s < NSET; ++s) {
+    if (bq == 0) {
+      fm[wave * 8 + s * 4 + jq] = m_run[s];
+      fl[wave * 8 + s * 4 + jq] = l_run[s];
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) fo[(wave * 8 + s * 4 + r) * kHeadDim + 64 * h + lane] = O[s][h][r];
+  }
+  __syncthreads();
+  float* os = fo + kWaves * 8 * kHeadDim;  // [G][128] merged output, rotated V domain
+  for (int i = tid; i < G * kHeadDim; i += kThreads) {
+    const int qh = i >> 7, dd = i & 127;
+    float mx = kNegInf;
+    for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, fm[w * 8 + qh]);
+    float l = 0.f, a = 0.f;
+    if (mx != kNegInf) {
+      for (int w = 0; w < kWaves; ++w) {
+        const float mw = fm[w * 8 + qh];
+        if (mw == kNegInf) continue;
+        const float e = exp2_hw(mw - mx);
+        l = fmaf(fl[w * 8 + qh], e, l);
+        a = fmaf(fo[(w * 8 + qh) * kHeadDim + dd], e, a);
+      }
+    }
+    if (n_splits == 1) {
+      os[i] = l > 0.f ? a / l : 0.f;
+    } else {
+      // device-coherent stores (no L2 write-back needed before the counter)
+      float* pb = part + ((static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits + split) * 130;
+      __hip_atomic_store(pb + 2 + dd, a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (dd == 0) {
+        __hip_atomic_store(pb, mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(pb + 1, l, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+
+  // ---------------- merge the splits (exact log-sum-exp) in the workgroup
+  // that finishes last; it resets the counter for the next call
+  if (n_splits > 1) {
+    // Every thread's partial stores complete (device-coherent) before the
+    // barrier; then one increment per workgroup.  The increment's return
+    // value gates the loads below, so they cannot run ahead of it.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __syncthreads();
+    if (tid == 0)
+      *last = __hip_atomic_fetch_add(counters + lz * d.n_kv + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+              n_splits - 1;
+    __syncthreads();
+    if (*last == 0) return;
+    for (int i = tid; i < G * kHeadDim; i += kThreads) {
+      const int qh = i >> 7, dd = i & 127;
+      const float* P = part + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits * 130;
+      const auto ld = [](const float* x) { return __hip_atomic_load(x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
+      // eight splits per round, their loads in flight together; running
+      // maximum with rescaling between rounds
+      float mx = kNegInf, l = 0.f, a = 0.f;
+      for (int sp0 = 0; sp0 < n_splits; sp0 += 8) {
+        float ms[8], ls[8], as[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          ms[u] = kNegInf;
+          ls[u] = as[u] = 0.f;
+          if (sp0 + u < n_splits) {
+            const float* ps = P + (sp0 + u) * 130;
+            ms[u] = ld(ps);
+            ls[u] = ld(ps + 1);
+            as[u] = ld(ps + 2 + dd);
+          }
+        }
+        float mc = mx;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) mc = fmaxf(mc, ms[u]);
+        if (mc == kNegInf) continue;
+        const float r = mx == kNegInf ? 0.f : exp2_hw(mx - mc);
+        l *= r;
+        a *= r;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (ms[u] == kNegInf) continue;
+          const float e = exp2_hw(ms[u] - mc);
+          l = fmaf(ls[u], e, l);
+          a = fmaf(as[u], e, a);
+        }
+        mx = mc;
+      }
+      os[i] = l > 0.f ? a / l : 0.f;
+    }
+    if (tid == 0) __hip_atomic_store(counters + lz * d.n_kv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  // ---------------- out = Pi_V^T o (back from the rotated V domain), or o
+  for (int i = tid; i < G * kHeadDim; i += kThreads) {
+    const int qh = i >> 7, dd = i & 127;
+    float r = os[i];
+    if (rotv != nullptr) {
+      r = 0.f;
+      for (int jj = 0; jj < kHeadDim; ++jj) r = fmaf(rotv[jj * kHeadDim + dd], os[qh * kHeadDim + jj], r);
+    }
+    out[(static_cast<size_t>(lz) * hqn + kvh * G + qh) * kHeadDim + dd] = r;
+  }
+}
+
 // ---------------------------------------------------------------- kernel
 template <int NSET, int KWB, int BV>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 16 ? 3 : 4))) void k_split_mfma(
@@ -529,7 +657,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: tile addresses stay scalar
-  const int bq = lane >> 2, jq = lane & 3;
+  const int bq = lane >> 2;
   // One-dimensional grid of (unit, split) items, units in the layout's
   // dispatch order (most expensive rows first, so that the second round of
   // workgroups fills in behind the long first ones); the splits of a unit
@@ -831,117 +959,225 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     pv_steps<BV, NSET>(std::make_integer_sequence<int, 16>{}, smem, vw, rep, pp, O);
   }
 
-#pragma unroll
-  for (int s = 0; s < NSET; ++s) l_run[s] = xsum16(l_run[s]);
+  finish_unit<NSET>(smem, reinterpret_cast<int*>(smem + kGmeta), d, G, lz, kvh, split, tid, lane, wave, m_run, l_run,
+                    O, counters, part, n_splits, reinterpret_cast<const float*>(blob + kOffRotV), out);
+}
 
-  // ---------------- merge the 8 waves of the workgroup
+// ---------------------------------------------------------------- fp16 comparator
+// The same split-context decode over an uncompressed fp16 cache (keys and
+// values [rows][128]): the same work mapping, MFMA products, softmax and
+// merges, with no decode and no rotation.  Keys: lane = token reads its
+// 256-byte row in four 64-byte chunks (8 steps each), the next chunk in
+// flight.  Values: lane = dim gathers each 4-token step with 2-byte loads
+// (every load instruction reads one row's 128 contiguous bytes), half of a
+// tile issued with its keys and the other half after its QK products.
+constexpr int kF16Flag = (kWaves * 8 * 2 + kWaves * 8 * kHeadDim + 8 * kHeadDim) * 4;  // past the merge area
+constexpr int kF16Lds = kF16Flag + 16;
+
+template <int NSET, int S0, int... J>
+__device__ __forceinline__ void f16_qk_chunk(std::integer_sequence<int, J...>, const uint4 (&ka)[4],
+                                             const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
+                                             float4_t (&L)[NSET]) {
+  (qk_mac<NSET, (S0 + J) % 16>((J & 1) ? as_half4(ka[J >> 1].z, ka[J >> 1].w) : as_half4(ka[J >> 1].x, ka[J >> 1].y),
+                               qh, ql, L),
+   ...);
+}
+
+template <int NSET, int S0, int... S>
+__device__ __forceinline__ void f16_pv(std::integer_sequence<int, S...>, const half4_t (&vv)[8][2],
+                                       const half4_t (&pp)[NSET], float4_t (&O)[NSET][2]) {
+  (
+      [&] {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int s = 0; s < NSET; ++s)
+            O[s][h] = __builtin_amdgcn_mfma_f32_4x4x4f16(pp[s], vv[S][h], O[s][h], 4, S0 + S, 0);
+      }(),
+      ...);
+}
+
+// values of steps S0 .. S0 + 7 of the tile at t0: vv[s][h] = the 4 tokens of
+// step S0 + s at dim 64 h + lane
+template <int S0>
+__device__ __forceinline__ void f16_load_values(const _Float16* vb, int t0, int lane, half4_t (&vv)[8][2]) {
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const _Float16* p = vb + static_cast<size_t>(t0 + 4 * (S0 + s)) * kHeadDim + 64 * h + lane;
+      half4_t v;
+      v[0] = p[0];
+      v[1] = p[kHeadDim];
+      v[2] = p[2 * kHeadDim];
+      v[3] = p[3 * kHeadDim];
+      vv[s][h] = v;
+    }
+}
+
+template <int NSET>
+__global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __restrict__ q,
+                                                       const int32_t* __restrict__ ctx_len,
+                                                       const _Float16* __restrict__ k16,
+                                                       const _Float16* __restrict__ v16, float* __restrict__ out,
+                                                       int32_t* __restrict__ counters, float* __restrict__ part,
+                                                       int n_splits, int split_len) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[kF16Lds];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int item = static_cast<int>(__builtin_amdgcn_workgroup_id_x());
+  const int split = item % n_splits, rest = item / n_splits;
+  const int kvh = rest % d.n_kv, lz = rest / d.n_kv;
+  const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
+  const int seq = lz % d.batch;
+  const int G = d.group, hqn = d.n_kv * G, cap = d.capacity;
+
+  // query image, 2 slots of 16 steps (as in the packed decode), logits in
+  // base-2 units: q / sqrt(d_h) * log2 e, fp16 hi and lo parts
+  static_assert(2 * 2 * 2 * 64 * 8 <= kF16Flag, "query image inside the merge area");
+  for (int i = tid; i < 2 * NSET * 64 * 4; i += kThreads) {
+    const int k = i & 3, l = (i >> 2) & 63, set = (i >> 8) % NSET, slot = (i >> 8) / NSET;
+    const int step = 16 * slot + (l >> 2), qh = 4 * set + (l & 3), coord = 4 * step + k;
+    float v = 0.f;
+    if (qh < G)
+      v = ld_q(q, (static_cast<size_t>(lz) * hqn + kvh * G + qh) * kHeadDim + coord, d.in_dtype) *
+          (kLog2e / 11.313708498984761f);
+    const _Float16 hi = static_cast<_Float16>(v);
+    const _Float16 lo = static_cast<_Float16>(v - static_cast<float>(hi));
+    uint8_t* dst = smem + (((slot * 2 + set) * 2) * 64 + l) * 8 + k * 2;
+    *reinterpret_cast<_Float16*>(dst) = hi;
+    *reinterpret_cast<_Float16*>(dst + 64 * 8) = lo;
+  }
   __syncthreads();
-  float* fm = reinterpret_cast<float*>(smem);            // [wave][8] max
-  float* fl = fm + kWaves * 8;                           // [wave][8] sum
-  float* fo = fl + kWaves * 8;                           // [wave][8][128] accumulators
+
+  const int ctx = min(ctx_len[seq], cap);
+  const int t_begin = split * split_len;
+  const int t_end = min(t_begin + split_len, ctx);
+  const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + kvh;
+  const _Float16* kb = k16 + row * cap * kHeadDim;
+  const _Float16* vb = v16 + row * cap * kHeadDim;
+  const uint32_t qlane = static_cast<uint32_t>(lane) * 8;
+
+  float m_run[NSET], l_run[NSET];
+  float4_t O[NSET][2];
 #pragma unroll
   for (int s = 0; s < NSET; ++s) {
-    if (bq == 0) {
-      fm[wave * 8 + s * 4 + jq] = m_run[s];
-      fl[wave * 8 + s * 4 + jq] = l_run[s];
-    }
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) fo[(wave * 8 + s * 4 + r) * kHeadDim + 64 * h + lane] = O[s][h][r];
+    m_run[s] = kNegInf;
+    l_run[s] = 0.f;
+    O[s][0] = O[s][1] = float4_t{0.f, 0.f, 0.f, 0.f};
   }
-  __syncthreads();
-  float* os = fo + kWaves * 8 * kHeadDim;  // [G][128] merged output, rotated V domain
-  for (int i = tid; i < G * kHeadDim; i += kThreads) {
-    const int qh = i >> 7, dd = i & 127;
-    float mx = kNegInf;
-    for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, fm[w * 8 + qh]);
-    float l = 0.f, a = 0.f;
-    if (mx != kNegInf) {
-      for (int w = 0; w < kWaves; ++w) {
-        const float mw = fm[w * 8 + qh];
-        if (mw == kNegInf) continue;
-        const float e = exp2_hw(mw - mx);
-        l = fmaf(fl[w * 8 + qh], e, l);
-        a = fmaf(fo[(w * 8 + qh) * kHeadDim + dd], e, a);
-      }
-    }
-    if (n_splits == 1) {
-      os[i] = l > 0.f ? a / l : 0.f;
-    } else {
-      // device-coherent stores (no L2 write-back needed before the counter)
-      float* pb = part + ((static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits + split) * 130;
-      __hip_atomic_store(pb + 2 + dd, a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (dd == 0) {
-        __hip_atomic_store(pb, mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(pb + 1, l, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
-  }
+  const int stride = kWaves * 64;
+  for (int t0 = t_begin + wave * 64; t0 < t_end; t0 += stride) {
+    // every row of the tile is below the capacity (a multiple of 64)
+    const uint4* kr = reinterpret_cast<const uint4*>(kb + static_cast<size_t>(t0 + lane) * kHeadDim);
+    uint4 ka[4], kn[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ka[j] = kr[j];
+    half4_t va[8][2];
+    f16_load_values<0>(vb, t0, lane, va);
 
-  // ---------------- merge the splits (exact log-sum-exp) in the workgroup
-  // that finishes last; it resets the counter for the next call
-  if (n_splits > 1) {
-    // Every thread's partial stores complete (device-coherent) before the
-    // barrier; then one increment per workgroup.  The increment's return
-    // value gates the loads below, so they cannot run ahead of it.
-    int* last = reinterpret_cast<int*>(smem + kGmeta);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __syncthreads();
-    if (tid == 0)
-      *last = __hip_atomic_fetch_add(counters + lz * d.n_kv + kvh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-              n_splits - 1;
-    __syncthreads();
-    if (*last == 0) return;
-    for (int i = tid; i < G * kHeadDim; i += kThreads) {
-      const int qh = i >> 7, dd = i & 127;
-      const float* P = part + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits * 130;
-      const auto ld = [](const float* x) { return __hip_atomic_load(x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
-      // eight splits per round, their loads in flight together; running
-      // maximum with rescaling between rounds
-      float mx = kNegInf, l = 0.f, a = 0.f;
-      for (int sp0 = 0; sp0 < n_splits; sp0 += 8) {
-        float ms[8], ls[8], as[8];
+    // ---------------- QK (lane = token), 4 chunks of 8 steps
+    float4_t L[NSET];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          ms[u] = kNegInf;
-          ls[u] = as[u] = 0.f;
-          if (sp0 + u < n_splits) {
-            const float* ps = P + (sp0 + u) * 130;
-            ms[u] = ld(ps);
-            ls[u] = ld(ps + 1);
-            as[u] = ld(ps + 2 + dd);
-          }
-        }
-        float mc = mx;
+    for (int s = 0; s < NSET; ++s) L[s] = float4_t{0.f, 0.f, 0.f, 0.f};
+    half4_t qh[NSET], ql[NSET];
+    const auto qslot = [&](int slot) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) mc = fmaxf(mc, ms[u]);
-        if (mc == kNegInf) continue;
-        const float r = mx == kNegInf ? 0.f : exp2_hw(mx - mc);
-        l *= r;
-        a *= r;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          if (ms[u] == kNegInf) continue;
-          const float e = exp2_hw(ms[u] - mc);
-          l = fmaf(ls[u], e, l);
-          a = fmaf(as[u], e, a);
-        }
-        mx = mc;
+      for (int s = 0; s < NSET; ++s) {
+        const uint32_t base = qlane + ((slot * 2 + s) * 2) * 64 * 8;
+        const uint2 uh = lds64(smem, base), ul = lds64(smem, base + 64 * 8);
+        qh[s] = as_half4(uh.x, uh.y);
+        ql[s] = as_half4(ul.x, ul.y);
       }
-      os[i] = l > 0.f ? a / l : 0.f;
+    };
+    const auto next = [&](int c) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) kn[j] = kr[4 * c + j];
+    };
+    const auto swap = [&]() {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) ka[j] = kn[j];
+    };
+    qslot(0);
+    next(1);
+    f16_qk_chunk<NSET, 0>(std::make_integer_sequence<int, 8>{}, ka, qh, ql, L);
+    swap();
+    next(2);
+    f16_qk_chunk<NSET, 8>(std::make_integer_sequence<int, 8>{}, ka, qh, ql, L);
+    swap();
+    next(3);
+    qslot(1);
+    f16_qk_chunk<NSET, 16>(std::make_integer_sequence<int, 8>{}, ka, qh, ql, L);
+    swap();
+    f16_qk_chunk<NSET, 24>(std::make_integer_sequence<int, 8>{}, ka, qh, ql, L);
+    half4_t vb2[8][2];
+    f16_load_values<8>(vb, t0, lane, vb2);
+
+    // ---------------- online softmax, as in the packed decode (value rows
+    // past the split end are zeroed: the cache there may hold anything)
+    const bool full = t0 + 64 <= t_end;
+    const int tk = t0 + lane;
+    if (!full) {
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (t0 + 4 * s + r >= t_end) va[s][0][r] = va[s][1][r] = static_cast<_Float16>(0.f);
+          if (t0 + 4 * (8 + s) + r >= t_end) vb2[s][0][r] = vb2[s][1][r] = static_cast<_Float16>(0.f);
+        }
     }
-    if (tid == 0) __hip_atomic_store(counters + lz * d.n_kv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    half4_t pp[NSET];
+#pragma unroll
+    for (int s = 0; s < NSET; ++s) {
+      float4_t x = L[s];
+      if (!full && tk >= t_end) x = float4_t{kNegInf, kNegInf, kNegInf, kNegInf};
+      quad_transpose(x, lane);
+      float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+      mx = xmax16(mx);
+      const float mn = fmaxf(m_run[s], mx);
+      const float corr = m_run[s] == kNegInf ? 0.f : exp2_hw(m_run[s] - mn);
+      float ps = 0.f;
+      uint32_t ph[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = exp2_hw(x[r] - mn);
+        ps += p;
+        ph[r] = __half_as_ushort(__float2half_rn(p));
+      }
+      pp[s] = as_half4(ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16));
+      l_run[s] = l_run[s] * corr + ps;
+      if (__builtin_amdgcn_ballot_w64(mn != m_run[s]) != 0) {
+        const float c0 = qperm<0x00>(corr), c1 = qperm<0x55>(corr), c2 = qperm<0xAA>(corr), c3 = qperm<0xFF>(corr);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          O[s][h][0] *= c0;
+          O[s][h][1] *= c1;
+          O[s][h][2] *= c2;
+          O[s][h][3] *= c3;
+        }
+      }
+      m_run[s] = mn;
+    }
+
+    // ---------------- PV (lane = dim), 16 steps of 4 tokens
+    f16_pv<NSET, 0>(std::make_integer_sequence<int, 8>{}, va, pp, O);
+    f16_pv<NSET, 8>(std::make_integer_sequence<int, 8>{}, vb2, pp, O);
   }
   __syncthreads();
-  // ---------------- back from the rotated V domain: out = Pi_V^T o
-  const float* rotv = reinterpret_cast<const float*>(blob + kOffRotV);
-  for (int i = tid; i < G * kHeadDim; i += kThreads) {
-    const int qh = i >> 7, dd = i & 127;
-    float r = 0.f;
-    for (int jj = 0; jj < kHeadDim; ++jj) r = fmaf(rotv[jj * kHeadDim + dd], os[qh * kHeadDim + jj], r);
-    out[(static_cast<size_t>(lz) * hqn + kvh * G + qh) * kHeadDim + dd] = r;
-  }
+  finish_unit<NSET>(smem, reinterpret_cast<int*>(smem + kF16Flag), d, G, lz, kvh, split, tid, lane, wave, m_run, l_run,
+                    O, counters, part, n_splits, nullptr, out);
+}
+
+inline hipError_t launch_f16_mfma_impl(const Dims& d, const void* q, const int32_t* ctx_len, const void* k16,
+                                       const void* v16, float* out, const DecodeWs& ws, hipStream_t s) {
+  dim3 grid(ws.n_splits * d.n_kv * d.batch * d.n_lc);
+  const auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, d, q, ctx_len, static_cast<const _Float16*>(k16),
+                       static_cast<const _Float16*>(v16), out, ws.counters, ws.part, ws.n_splits, ws.split_len);
+  };
+  if (d.group <= 4) go(k_f16_mfma<1>);
+  else go(k_f16_mfma<2>);
+  return hipGetLastError();
 }
 
 // Launch the packed decode for value width BV (one instantiation per file).

@@ -3,8 +3,8 @@
 //  k_quantize      : TQ-MSE encode (Sec. 2.2) of appended K rows per same-rate
 //                    group (end of Sec. 3.2) and of V rows, dense b-bit pack.
 //  (the packed-cache decode lives in decode_impl.h)
-//  k_merge         : exact log-sum-exp merge of the splits + inverse V rotation.
-//  k_split_fp16    : the same decode over an fp16 cache (comparator).
+//  k_append_rows   : the same encode for appends of a few rows (decode steps).
+//  (the fp16 comparator decode lives in decode_impl.h too)
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -28,12 +28,6 @@ __device__ __forceinline__ float ld_in(const void* p, size_t i, int dtype) {
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
   return v;
 }
 
@@ -436,149 +430,6 @@ __global__ __launch_bounds__(1024) void k_append_rows(Dims d, const uint8_t* __r
   }
 }
 
-// ---------------------------------------------------------------------------
-// fp16 comparator: same split structure over an uncompressed fp16 cache.
-// ---------------------------------------------------------------------------
-template <int G>
-__global__ __launch_bounds__(256) void k_split_fp16(Dims d, const void* __restrict__ q,
-                                                    const int32_t* __restrict__ ctx_len,
-                                                    const __half* __restrict__ k16,
-                                                    const __half* __restrict__ v16,
-                                                    float* __restrict__ part, int n_splits,
-                                                    int split_len) {
-  __shared__ float sq[G][kHeadDim];
-  __shared__ float pt[G][256];
-  __shared__ float red[2][G][4];
-  __shared__ float xch[G][kHeadDim];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int split = blockIdx.x, kvh = blockIdx.y, lz = blockIdx.z;
-  const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
-  const int seq = lz % d.batch;
-  const int hqn = d.n_kv * G;
-  const int cap = d.capacity;
-  const float qscale = 1.0f / sqrtf(static_cast<float>(kHeadDim));
-  for (int i = tid; i < G * kHeadDim; i += 256)
-    sq[i >> 7][i & 127] =
-        ld_in(q, (static_cast<size_t>(lz) * hqn + kvh * G + (i >> 7)) * kHeadDim + (i & 127), d.in_dtype) * qscale;
-  __syncthreads();
-
-  const int ctx = min(ctx_len[seq], cap);
-  const int t0 = split * split_len;
-  const int t1 = min(t0 + split_len, ctx);
-  const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + kvh;
-  const __half* kb = k16 + row * cap * kHeadDim;
-  const __half* vb = v16 + row * cap * kHeadDim;
-
-  float m_run[G], l_run[G], acc[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m_run[h] = kNegInf;
-    l_run[h] = 0.f;
-    acc[h] = 0.f;
-  }
-  const int j = tid & 127, half = tid >> 7;
-  for (int c0 = t0; c0 < t1; c0 += 256) {
-    const int nrow = min(256, t1 - c0);
-    const bool valid = tid < nrow;
-    float lg[G];
-    if (valid) {
-#pragma unroll
-      for (int h = 0; h < G; ++h) lg[h] = 0.f;
-      const __half2* kr = reinterpret_cast<const __half2*>(kb + static_cast<size_t>(c0 + tid) * kHeadDim);
-      for (int p2 = 0; p2 < kHeadDim / 2; ++p2) {
-        const float2 kv = __half22float2(kr[p2]);
-#pragma unroll
-        for (int h = 0; h < G; ++h) lg[h] = fmaf(sq[h][2 * p2], kv.x, fmaf(sq[h][2 * p2 + 1], kv.y, lg[h]));
-      }
-    } else {
-#pragma unroll
-      for (int h = 0; h < G; ++h) lg[h] = kNegInf;
-    }
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mx = wave_max(lg[h]);
-      if (lane == 0) red[0][h][wave] = mx;
-    }
-    __syncthreads();
-    float corr[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mt = fmaxf(fmaxf(red[0][h][0], red[0][h][1]), fmaxf(red[0][h][2], red[0][h][3]));
-      const float mn = fmaxf(m_run[h], mt);
-      corr[h] = m_run[h] == kNegInf ? 0.f : __expf(m_run[h] - mn);
-      const float p = valid ? __expf(lg[h] - mn) : 0.f;
-      pt[h][tid] = p;
-      const float ps = wave_sum(p);
-      if (lane == 0) red[1][h][wave] = ps;
-      m_run[h] = mn;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      l_run[h] = l_run[h] * corr[h] + (red[1][h][0] + red[1][h][1] + red[1][h][2] + red[1][h][3]);
-      acc[h] *= corr[h];
-    }
-    const int s_end = min(half * 128 + 128, nrow);
-    for (int s = half * 128; s < s_end; ++s) {
-      const float val = __half2float(vb[static_cast<size_t>(c0 + s) * kHeadDim + j]);
-#pragma unroll
-      for (int h = 0; h < G; ++h) acc[h] = fmaf(pt[h][s], val, acc[h]);
-    }
-    __syncthreads();
-  }
-  if (half == 1) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) xch[h][j] = acc[h];
-  }
-  __syncthreads();
-  if (half == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float* pb = part + ((static_cast<size_t>(lz) * hqn + kvh * G + h) * n_splits + split) * 130;
-      pb[2 + j] = acc[h] + xch[h][j];
-      if (j == 0) {
-        pb[0] = m_run[h];
-        pb[1] = l_run[h];
-      }
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Exact LSE merge over splits, then out = Pi_V^T o_rot (if rotv != null).
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(128) void k_merge(Dims d, const float* __restrict__ part, int n_splits,
-                                               const float* __restrict__ rotv, float* __restrict__ out) {
-  __shared__ float os[kHeadDim];
-  const int tid = threadIdx.x;
-  const int hq = blockIdx.x, seq = blockIdx.y, lc = blockIdx.z;
-  const int hqn = d.n_kv * d.group;
-  const size_t lz = static_cast<size_t>(lc) * d.batch + seq;
-  const float* P = part + (lz * hqn + hq) * n_splits * 130;
-  float mx = kNegInf;
-  for (int s = 0; s < n_splits; ++s) mx = fmaxf(mx, P[s * 130]);
-  float l = 0.f, a = 0.f;
-  if (mx != kNegInf) {
-    for (int s = 0; s < n_splits; ++s) {
-      const float ms = P[s * 130];
-      if (ms == kNegInf) continue;
-      const float e = __expf(ms - mx);
-      l = fmaf(P[s * 130 + 1], e, l);
-      a = fmaf(P[s * 130 + 2 + tid], e, a);
-    }
-  }
-  const float o = l > 0.f ? a / l : 0.f;
-  float r = o;
-  if (rotv != nullptr) {
-    os[tid] = o;
-    __syncthreads();
-    r = 0.f;
-    for (int jj = 0; jj < kHeadDim; ++jj) r = fmaf(rotv[jj * kHeadDim + tid], os[jj], r);
-  }
-  out[(lz * hqn + hq) * kHeadDim + tid] = r;
-}
-
 }  // namespace
 
 hipError_t launch_quantize_append(const Dims& d, const void* layout, const void* k, const void* v,
@@ -612,32 +463,5 @@ hipError_t launch_decode_packed(const Dims& d, const void* layout, const void* q
   }
 }
 
-template <int G>
-static void launch_split_fp16_g(const Dims& d, const void* q, const int32_t* ctx, const void* k16,
-                                const void* v16, const DecodeWs& ws, hipStream_t s) {
-  dim3 grid(ws.n_splits, d.n_kv, d.batch * d.n_lc);
-  hipLaunchKernelGGL(k_split_fp16<G>, grid, dim3(256), 0, s, d, q, ctx,
-                     static_cast<const __half*>(k16), static_cast<const __half*>(v16), ws.part,
-                     ws.n_splits, ws.split_len);
-}
-
-hipError_t launch_decode_fp16(const Dims& d, const void* q, const int32_t* ctx_len, const void* k16,
-                              const void* v16, float* out, const DecodeWs& ws, hipStream_t s) {
-  switch (d.group) {
-    case 1: launch_split_fp16_g<1>(d, q, ctx_len, k16, v16, ws, s); break;
-    case 2: launch_split_fp16_g<2>(d, q, ctx_len, k16, v16, ws, s); break;
-    case 3: launch_split_fp16_g<3>(d, q, ctx_len, k16, v16, ws, s); break;
-    case 4: launch_split_fp16_g<4>(d, q, ctx_len, k16, v16, ws, s); break;
-    case 5: launch_split_fp16_g<5>(d, q, ctx_len, k16, v16, ws, s); break;
-    case 6: launch_split_fp16_g<6>(d, q, ctx_len, k16, v16, ws, s); break;
-    case 7: launch_split_fp16_g<7>(d, q, ctx_len, k16, v16, ws, s); break;
-    case 8: launch_split_fp16_g<8>(d, q, ctx_len, k16, v16, ws, s); break;
-    default: return hipErrorInvalidValue;
-  }
-  const int hqn = d.n_kv * d.group;
-  hipLaunchKernelGGL(k_merge, dim3(hqn, d.batch, d.n_lc), dim3(128), 0, s, d, ws.part, ws.n_splits,
-                     static_cast<const float*>(nullptr), out);
-  return hipGetLastError();
-}
 
 }  // namespace bgtq

@@ -245,6 +245,39 @@ def test_small_appends_cross_tiles_and_value_words():
     assert stats.code_ties <= 1e-4 * stats.codes
 
 
+def test_fp16_comparator_group8_ragged_and_poisoned_tail():
+    """The fp16 comparator decode (MFMA kernel) with G = 8 query heads per KV
+    head, ragged contexts that end inside a tile, several splits, and NaN in
+    every cache row past the context (masked scores, zeroed values)."""
+    bg = bgm()
+    cfg = bg.Config(n_layers=2, batch=2, n_kv_heads=2, group=8, capacity=320, k_budget=192, v_bits=3,
+                    in_dtype=bg.BGTQ_BF16)
+    rng = np.random.default_rng(11)
+    k = rng.standard_normal((2, 2, 2, 320, 128)).astype(np.float16)
+    v = rng.standard_normal((2, 2, 2, 320, 128)).astype(np.float16)
+    ctxl = [261, 77]
+    for b in range(2):
+        k[:, b, :, ctxl[b]:] = np.nan
+        v[:, b, :, ctxl[b]:] = np.nan
+    q = synth.cast(rng.standard_normal((2, 2, 16, 128)), "bf16")
+    k16 = torch.from_numpy(k).cuda()
+    v16 = torch.from_numpy(v).cuda()
+    ctx = torch.tensor(ctxl, dtype=torch.int32, device="cuda")
+    for layer in (-1, 1):
+        for ns in (0, 3):
+            qq = q if layer < 0 else q[layer]
+            out = bg.blockgtq_decode_attn_fp16(cfg, layer, to_dev(np.ascontiguousarray(qq), "bf16"), ctx, max(ctxl),
+                                               k16, v16, n_splits=ns).cpu().numpy().astype(np.float64)
+            for li in ([0, 1] if layer < 0 else [1]):
+                for b in range(2):
+                    for h in range(2):
+                        got = (out[li] if layer < 0 else out)[b, h * 8:(h + 1) * 8]
+                        ref = o.attention(q[li, b, h * 8:(h + 1) * 8], k[li, b, h, :ctxl[b]].astype(np.float64),
+                                          v[li, b, h, :ctxl[b]].astype(np.float64))
+                        assert np.all(np.isfinite(got))
+                        assert P.rel_err(got, ref) <= 2e-3, (layer, ns, li, b, h)
+
+
 def test_all_layers_launch_matches_per_layer_and_split_invariance():
     bg = bgm()
     st = P.make_setup(5, 3, 2, 2, 4, 1024, 128, 2, 1e4, "bf16", n_cal=128)
