@@ -60,6 +60,14 @@ constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLog2e = 1.4426950408889634f;
 // 2^x (the hardware exponential; arguments here are <= 0)
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+// fp16(p0 lo(w)) | fp16(p1 hi(w)) << 16, w = two fp16: one mixed-precision
+// fused product into each half (single rounding to fp16)
+__device__ __forceinline__ uint32_t mix_pair(float p0, float p1, uint32_t w) {
+  uint32_t r;
+  asm("v_fma_mixlo_f16 %0, %1, %2, 0 op_sel_hi:[0,1,0]" : "=v"(r) : "v"(p0), "v"(w));
+  asm("v_fma_mixhi_f16 %0, %1, %2, 0 op_sel:[0,1,0] op_sel_hi:[0,1,0]" : "+v"(r) : "v"(p1), "v"(w));
+  return r;
+}
 
 // LDS map (bytes).  The b = 2 table has 32 replicas at a 256-byte entry
 // stride: the lanes of a half-wave read 32 distinct banks, and the address is
@@ -524,14 +532,14 @@ __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const
 // Merge of the waves' (max, sum, accumulator) states in LDS, then (n_splits
 // > 1) of the splits of the unit in the workgroup that finishes it last
 // (exact log-sum-exp; it resets the unit's counter), then out = R^T o with R
-// the V rotation (rotv) or none.  The merge area of LDS starts at smem;
-// `last` is a flag word outside it.
+// the V rotation (rotv) or none, o scaled by oscale.  The merge area of LDS
+// starts at smem; `last` is a flag word outside it.
 template <int NSET>
 __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims& d, int G, int lz, int kvh,
                                             int split, int tid, int lane, int wave, float (&m_run)[NSET],
                                             float (&l_run)[NSET], const float4_t (&O)[NSET][2],
                                             int32_t* __restrict__ counters, float* __restrict__ part, int n_splits,
-                                            const float* __restrict__ rotv, float* __restrict__ out) {
+                                            float oscale, const float* __restrict__ rotv, float* __restrict__ out) {
   const int hqn = d.n_kv * G;
   const int bq = lane >> 2, jq = lane & 3;
 #pragma unroll
@@ -570,7 +578,7 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
       }
     }
     if (n_splits == 1) {
-      os[i] = l > 0.f ? a / l : 0.f;
+      os[i] = l > 0.f ? a / l * oscale : 0.f;
     } else {
       // device-coherent stores (no L2 write-back needed before the counter)
       float* pb = part + ((static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits + split) * 130;
@@ -631,7 +639,7 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
         }
         mx = mc;
       }
-      os[i] = l > 0.f ? a / l : 0.f;
+      os[i] = l > 0.f ? a / l * oscale : 0.f;
     }
     if (tid == 0) __hip_atomic_store(counters + lz * d.n_kv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -857,7 +865,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   const int t_begin = split * split_len;
   const int t_end = min(t_begin + split_len, ctx);
   const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + kvh;
-  const float vscale = 0.08838834764831845f;  // 1/sqrt(128)
 
   float m_run[NSET], l_run[NSET];
   float4_t O[NSET][2];
@@ -913,12 +920,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     // tile that reaches past the split end masks anything: its scores past
     // the end become -inf and their value radii 0.
     const bool full = t0 + 64 <= t_end;
-    float vn4[4] = {h2f(vn.x & 0xFFFFu) * vscale, h2f(vn.x >> 16) * vscale, h2f(vn.y & 0xFFFFu) * vscale,
-                    h2f(vn.y >> 16) * vscale};
+    // value radii stay packed fp16: p n_V is one mixed-precision product
+    // into each half of the PV operand (the codes' 1/sqrt(d_h) scales the
+    // output instead)
+    uint2 vr = vn;
     if (!full) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (t0 + 4 * bq + r >= t_end) vn4[r] = 0.f;
+      const int e = t_end - (t0 + 4 * bq);  // radii of tokens >= e are cleared
+      vr.x &= e <= 0 ? 0u : (e == 1 ? 0xFFFFu : 0xFFFFFFFFu);
+      vr.y &= e <= 2 ? 0u : (e == 3 ? 0xFFFFu : 0xFFFFFFFFu);
     }
     half4_t pp[NSET];
 #pragma unroll
@@ -931,14 +940,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
       const float mn = fmaxf(m_run[s], mx);
       const float corr = m_run[s] == kNegInf ? 0.f : exp2_hw(m_run[s] - mn);
       float ps = 0.f;
-      uint32_t ph[4];
+      float p[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = exp2_hw(x[r] - mn);
-        ps += p;
-        ph[r] = __half_as_ushort(__float2half_rn(p * vn4[r]));
+        p[r] = exp2_hw(x[r] - mn);
+        ps += p[r];
       }
-      pp[s] = as_half4(ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16));
+      pp[s] = as_half4(mix_pair(p[0], p[1], vr.x), mix_pair(p[2], p[3], vr.y));
       l_run[s] = l_run[s] * corr + ps;  // this lane's tokens only; reduced after the loop
       // the accumulators are rescaled only when some running maximum moved
       // (otherwise corr is exactly 1); the test is one wave-wide vote
@@ -960,7 +968,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   }
 
   finish_unit<NSET>(smem, reinterpret_cast<int*>(smem + kGmeta), d, G, lz, kvh, split, tid, lane, wave, m_run, l_run,
-                    O, counters, part, n_splits, reinterpret_cast<const float*>(blob + kOffRotV), out);
+                    O, counters, part, n_splits, 0.08838834764831845f /* 1/sqrt(d_h) */,
+                    reinterpret_cast<const float*>(blob + kOffRotV), out);
 }
 
 // ---------------------------------------------------------------- fp16 comparator
@@ -1137,14 +1146,14 @@ __global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __res
       const float mn = fmaxf(m_run[s], mx);
       const float corr = m_run[s] == kNegInf ? 0.f : exp2_hw(m_run[s] - mn);
       float ps = 0.f;
-      uint32_t ph[4];
+      half4_t ph;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const float p = exp2_hw(x[r] - mn);
         ps += p;
-        ph[r] = __half_as_ushort(__float2half_rn(p));
+        ph[r] = static_cast<_Float16>(p);
       }
-      pp[s] = as_half4(ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16));
+      pp[s] = ph;
       l_run[s] = l_run[s] * corr + ps;
       if (__builtin_amdgcn_ballot_w64(mn != m_run[s]) != 0) {
         const float c0 = qperm<0x00>(corr), c1 = qperm<0x55>(corr), c2 = qperm<0xAA>(corr), c3 = qperm<0xFF>(corr);
@@ -1165,7 +1174,7 @@ __global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __res
   }
   __syncthreads();
   finish_unit<NSET>(smem, reinterpret_cast<int*>(smem + kF16Flag), d, G, lz, kvh, split, tid, lane, wave, m_run, l_run,
-                    O, counters, part, n_splits, nullptr, out);
+                    O, counters, part, n_splits, 1.f, nullptr, out);
 }
 
 inline hipError_t launch_f16_mfma_impl(const Dims& d, const void* q, const int32_t* ctx_len, const void* k16,
