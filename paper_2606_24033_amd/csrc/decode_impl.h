@@ -73,15 +73,22 @@ __device__ __forceinline__ uint32_t mix_pair(float p0, float p1, uint32_t w) {
 // stride: the lanes of a half-wave read 32 distinct banks, and the address is
 // one byte permute of (code byte, replica offset).  Other entry strides: 128 B
 // for the 16- and 32-replica tables, 32 B for the 8-replica b = 4 table, 2 B
-// for the plain b >= 6 tables.
+// for the plain b >= 6 tables.  Every table starts at a multiple of its own
+// size, so an address is (entry << stride) | (table base + replica offset):
+// one shift and one and-or per lookup.
 constexpr int kLut2 = 0;                        // b=2: 256 entries (4 codes) x 32 replicas x 8 B
-constexpr int kLut1 = kLut2 + 256 * 256;        // b=1: 16 entries (4 codes) x 16 replicas x 8 B
-constexpr int kLut3 = kLut1 + 16 * 16 * 8;      // b=3: 64 (2 codes) x 32 x 4
+constexpr int kLut1B = kLut2 + 256 * 256;       // b=1 keys: 256 entries (8 codes) x 8 replicas x 16 B
+constexpr int kLut3 = kLut1B + 256 * 8 * 16;    // b=3: 64 (2 codes) x 32 x 4
 constexpr int kLut4 = kLut3 + 64 * 32 * 4;      // b=4: 256 (2 codes) x 8 x 4
 constexpr int kLut5 = kLut4 + 256 * 8 * 4;      // b=5: 32 (1 code, low half) x 32 x 4
-constexpr int kLutF = kLut5 + 32 * 32 * 4;      // b=6,7,8: plain fp16 tables at +0, +128, +384
-constexpr int kLut1B = kLutF + 1024;            // b=1 keys: 256 entries (8 codes) x 8 replicas x 16 B
-constexpr int kQimg = kLut1B + 256 * 8 * 16;    // [slot][set][hi,lo][lane] x 8 B
+constexpr int kLut1 = kLut5 + 32 * 32 * 4;      // b=1 values: 16 entries (4 codes) x 16 replicas x 8 B
+constexpr int kLutF = kLut1 + 16 * 16 * 8;      // b=8,7,6: plain fp16 tables at +0, +512, +768
+constexpr int kQimg = kLutF + 1024;             // [slot][set][hi,lo][lane] x 8 B
+static_assert(kLut1B % 32768 == 0 && kLut3 % 8192 == 0 && kLut4 % 8192 == 0 && kLut5 % 4096 == 0 &&
+                  kLut1 % 2048 == 0 && kLutF % 1024 == 0,
+              "table alignment");
+template <int B>
+constexpr int lutf_base() { return kLutF + (B == 8 ? 0 : (B == 7 ? 512 : 768)); }
 constexpr int kQimgBytes = kMaxSlots * 2 * 2 * 64 * 8;
 constexpr int kGmeta = kQimg + kQimgBytes;      // flag word of the split merge
 constexpr int kCbStage = kGmeta + 64;           // fp16 codebooks, staged for the table build
@@ -192,31 +199,32 @@ __device__ __forceinline__ float xsum16(float v) {
   return a + b;
 }
 
-// Bits [POS, POS + LEN) of the little-endian word array w (LEN <= 32).
-template <int POS, int LEN, int N>
-__device__ __forceinline__ uint32_t field(const uint32_t (&w)[N]) {
+// Bits [POS, POS + LEN) of the little-endian word array w, placed at bit SH
+// (other bits zero): one shift (or funnel shift) and one mask.
+template <int POS, int LEN, int SH, int N>
+__device__ __forceinline__ uint32_t field_at(const uint32_t (&w)[N]) {
   constexpr int wi = POS / 32, sh = POS % 32;
-  static_assert(wi < N, "field word");
+  static_assert(wi < N && SH + LEN <= 32, "field");
   uint32_t v;
-  if constexpr (sh == 0) {
-    v = w[wi];
-  } else if constexpr (sh + LEN <= 32) {
-    v = w[wi] >> sh;
+  if constexpr (sh + LEN > 32) {
+    static_assert(wi + 1 < N && sh >= SH, "field word");
+    v = __builtin_amdgcn_alignbit(w[wi + 1], w[wi], sh - SH);
+  } else if constexpr (sh >= SH) {
+    v = w[wi] >> (sh - SH);
   } else {
-    static_assert(wi + 1 < N, "field word");
-    v = __builtin_amdgcn_alignbit(w[wi + 1], w[wi], sh);
+    v = w[wi] << (SH - sh);
   }
-  if constexpr (LEN < 32) v &= (1u << LEN) - 1u;
-  return v;
+  return v & (((1u << LEN) - 1u) << SH);
 }
 
-// Per-lane replica offsets of the lookup tables.
+// Per-lane table base + replica offset of each lookup table.
 struct LaneRep {
-  uint32_t r16;  // (lane & 15) * 8
-  uint32_t r32;  // (lane & 31) * 4
-  uint32_t r8;   // (lane & 7) * 4
-  uint32_t r2;   // (lane & 31) * 8: replica offset in the b = 2 table
-  uint32_t r1b;  // (lane & 7) * 16: replica offset in the 8-code b = 1 table
+  uint32_t r1;   // kLut1 + (lane & 15) * 8
+  uint32_t r3;   // kLut3 + (lane & 31) * 4
+  uint32_t r4;   // kLut4 + (lane & 7) * 4
+  uint32_t r5;   // kLut5 + (lane & 31) * 4
+  uint32_t r2;   // kLut2 + (lane & 31) * 8
+  uint32_t r1b;  // kLut1B + (lane & 7) * 16
   uint32_t qimg; // kQimg + lane * 8: this lane's entry in slot 0 of the query image
 };
 
@@ -232,28 +240,25 @@ __device__ __forceinline__ uint32_t lut2_addr(uint32_t w, uint32_t r2) {
 template <int B, int POS, int N>
 __device__ __forceinline__ half4_t decode4(const uint8_t* smem, const uint32_t (&w)[N], const LaneRep& r) {
   if constexpr (B == 2 && POS % 8 == 0) {
-    const uint2 u = lds64(smem, kLut2 + lut2_addr<(POS % 32) / 8>(w[POS / 32], r.r2));
+    const uint2 u = lds64(smem, lut2_addr<(POS % 32) / 8>(w[POS / 32], r.r2));
     return as_half4(u.x, u.y);
   } else if constexpr (B == 2) {
-    const uint2 u = lds64(smem, kLut2 + r.r2 + (field<POS, 8>(w) << 8));
+    const uint2 u = lds64(smem, field_at<POS, 8, 8>(w) | r.r2);
     return as_half4(u.x, u.y);
   } else if constexpr (B == 1) {
-    const uint2 u = lds64(smem, kLut1 + r.r16 + (field<POS, 4>(w) << 7));
+    const uint2 u = lds64(smem, field_at<POS, 4, 7>(w) | r.r1);
     return as_half4(u.x, u.y);
   } else if constexpr (B == 3) {
-    return as_half4(lds32(smem, kLut3 + r.r32 + (field<POS, 6>(w) << 7)),
-                    lds32(smem, kLut3 + r.r32 + (field<POS + 6, 6>(w) << 7)));
+    return as_half4(lds32(smem, field_at<POS, 6, 7>(w) | r.r3), lds32(smem, field_at<POS + 6, 6, 7>(w) | r.r3));
   } else if constexpr (B == 4) {
-    return as_half4(lds32(smem, kLut4 + r.r8 + (field<POS, 8>(w) << 5)),
-                    lds32(smem, kLut4 + r.r8 + (field<POS + 8, 8>(w) << 5)));
+    return as_half4(lds32(smem, field_at<POS, 8, 5>(w) | r.r4), lds32(smem, field_at<POS + 8, 8, 5>(w) | r.r4));
   } else {
     constexpr int LS = B == 5 ? 7 : 1;
-    constexpr int base = B == 5 ? kLut5 : (B == 6 ? kLutF : (B == 7 ? kLutF + 128 : kLutF + 384));
-    const uint32_t rb = B == 5 ? r.r32 : 0u;
-    const uint32_t c0 = lds16(smem, base + rb + (field<POS, B>(w) << LS));
-    const uint32_t c1 = lds16(smem, base + rb + (field<POS + B, B>(w) << LS));
-    const uint32_t c2 = lds16(smem, base + rb + (field<POS + 2 * B, B>(w) << LS));
-    const uint32_t c3 = lds16(smem, base + rb + (field<POS + 3 * B, B>(w) << LS));
+    const uint32_t rb = B == 5 ? r.r5 : static_cast<uint32_t>(lutf_base<B>());
+    const uint32_t c0 = lds16(smem, field_at<POS, B, LS>(w) | rb);
+    const uint32_t c1 = lds16(smem, field_at<POS + B, B, LS>(w) | rb);
+    const uint32_t c2 = lds16(smem, field_at<POS + 2 * B, B, LS>(w) | rb);
+    const uint32_t c3 = lds16(smem, field_at<POS + 3 * B, B, LS>(w) | rb);
     return as_half4(c0 | (c1 << 16), c2 | (c3 << 16));
   }
 }
@@ -297,10 +302,8 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
     // leaving out their lo products moves the attention output by ~1e-4
     // (relative), against ~1e-3 for leaving out every lo product.
     constexpr int by = k / 2;  // byte of step k
-    const uint4 u01 = *reinterpret_cast<const uint4*>(
-        smem + kLut1B + ((__builtin_amdgcn_ubfe(aw[by / 4], 8 * (by % 4), 8) << 7) | rep.r1b));
-    const uint4 u23 = *reinterpret_cast<const uint4*>(
-        smem + kLut1B + ((__builtin_amdgcn_ubfe(aw[(by + 1) / 4], 8 * ((by + 1) % 4), 8) << 7) | rep.r1b));
+    const uint4 u01 = *reinterpret_cast<const uint4*>(smem + (field_at<8 * by, 8, 7>(aw) | rep.r1b));
+    const uint4 u23 = *reinterpret_cast<const uint4*>(smem + (field_at<8 * (by + 1), 8, 7>(aw) | rep.r1b));
     half4_t kv0 = as_half4(u01.x, u01.y), kv1 = as_half4(u01.z, u01.w);
     half4_t kv2 = as_half4(u23.x, u23.y), kv3 = as_half4(u23.z, u23.w);
     asm volatile("" : "+v"(kv0), "+v"(kv1), "+v"(kv2), "+v"(kv3));
@@ -849,17 +852,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   for (int i = tid; i < 32 * 32; i += kThreads)
     *reinterpret_cast<uint32_t*>(smem + kLut5 + i * 4) = cbs[cb_index(5) + (i >> 5)];
 #pragma unroll
-  for (int i = tid; i < 64 + 128 + 256; i += kThreads) {
-    const int b = i < 64 ? 6 : (i < 192 ? 7 : 8);
-    const int k = i < 64 ? i : (i < 192 ? i - 64 : i - 192);
+  for (int i = tid; i < 256 + 128 + 64; i += kThreads) {
+    const int b = i < 256 ? 8 : (i < 384 ? 7 : 6);
+    const int k = i < 256 ? i : (i < 384 ? i - 256 : i - 384);
     *reinterpret_cast<uint16_t*>(smem + kLutF + i * 2) = cbs[cb_index(b) + k];
   }
   __syncthreads();
 
   uint32_t gmb[8];
-  const LaneRep rep{static_cast<uint32_t>(lane & 15) * 8u, static_cast<uint32_t>(lane & 31) * 4u,
-                    static_cast<uint32_t>(lane & 7) * 4u, static_cast<uint32_t>(lane & 31) * 8u,
-                    static_cast<uint32_t>(lane & 7) * 16u, static_cast<uint32_t>(kQimg + lane * 8)};
+  LaneRep rep{static_cast<uint32_t>(kLut1 + (lane & 15) * 8), static_cast<uint32_t>(kLut3 + (lane & 31) * 4),
+                    static_cast<uint32_t>(kLut4 + (lane & 7) * 4),   static_cast<uint32_t>(kLut5 + (lane & 31) * 4),
+                    static_cast<uint32_t>(kLut2 + (lane & 31) * 8),  static_cast<uint32_t>(kLut1B + (lane & 7) * 16),
+                    static_cast<uint32_t>(kQimg + lane * 8)};
+  // opaque to the compiler: with the bits of the bases unknown, a lookup
+  // address stays (shifted field & mask) | base, one and-or
+  asm volatile("" : "+v"(rep.r1), "+v"(rep.r3), "+v"(rep.r4), "+v"(rep.r5), "+v"(rep.r2), "+v"(rep.r1b));
 
   const int ctx = min(ctx_len[seq], cap);
   const int t_begin = split * split_len;
