@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--n-splits", type=int, default=0)
     ap.add_argument("--no-fp16", action="store_true", help="skip the fp16 comparator")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-uniform", action="store_true",
+                    help="skip the uniform TQ-MSE K layout (one K group per head) comparison")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one plain device copy of this size first (HBM counter calibration)")
@@ -131,6 +133,47 @@ def cpu_oracle_baseline(bits, sig, rot_k, rot_v, T, budget_s):
             "sample": f"{units} of {N_LAYERS * N_KV} (layer, KV head) units of one decode step at ctx {T + 1} "
                       f"(encode appended row + rotated-form fp64 attention), {elapsed:.1f} s",
             "us_per_step_equiv": elapsed / units * N_LAYERS * N_KV * 1e6}
+
+
+def uniform_comparison(bg, synth, torch, cfg, rot_k, rot_v, sig, T, n_extra, q_all, ctxs, max_ctx, ws, args,
+                       ctx_mean, dec_med, f16_us):
+    """The same decode over a uniform TQ-MSE K layout: every RoPE block at
+    K_BUDGET / 64 bits, i.e. one K group of 128 coordinates and one K radius
+    per row (the paper's uniform-TQ-MSE baseline, which differs from Block-GTQ
+    only in the K layout).  Decode calls only, at the timed steps' contexts,
+    over a cache prefilled with all their rows."""
+    ubits = np.full((N_LAYERS, N_KV, 64), K_BUDGET // 64, np.uint8)
+    ulayout = bg.Layout(cfg, ubits, synth.flat_rot_k(rot_k), rot_v)
+    ucache = bg.Cache(cfg)
+    wp0 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for layer in range(N_LAYERS):
+        k, v = synth.torch_layer_kv(SEED, layer, T + n_extra, sig[layer], BASE)
+        bg.blockgtq_quantize_append(cfg, ulayout, layer, k[None].contiguous(), v[None].contiguous(), wp0, ucache)
+        del k, v
+    uout = torch.empty((N_LAYERS, 1, N_KV * GROUP, 128), dtype=torch.float32, device="cuda")
+    for i in range(args.warmup):
+        s = args.warmup + i % args.steps
+        bg.blockgtq_decode_attn(cfg, ulayout, -1, q_all[s], ctxs[s:s + 1], max_ctx, ucache, out=uout, workspace=ws,
+                                n_splits=args.n_splits)
+    ue = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for i in range(args.steps):
+        s = args.warmup + i
+        ue[i][0].record()
+        bg.blockgtq_decode_attn(cfg, ulayout, -1, q_all[s], ctxs[s:s + 1], max_ctx, ucache, out=uout, workspace=ws,
+                                n_splits=args.n_splits)
+        ue[i][1].record()
+    torch.cuda.synchronize()
+    u_us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in ue]))
+    ubytes = ctx_mean * N_LAYERS * N_KV * (K_BUDGET * 2 / 8 + 2 + 128 * V_BITS / 8 + 2) + \
+        N_LAYERS * N_KV * GROUP * 128 * (2 + 4)
+    res = {"decode_us_median": round(u_us, 2), "bytes_per_call": int(ubytes),
+           "gbs": round(ubytes / (u_us * 1e-6) / 1e9, 2),
+           "pct_hbm_peak": round(100 * ubytes / (u_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 2),
+           "block_gtq_time_over_uniform": round(dec_med / u_us, 3)}
+    if f16_us is not None:
+        res["speedup_vs_fp16_decode"] = round(f16_us / u_us, 3)
+    del ucache, ulayout
+    return res
 
 
 def main():
@@ -285,6 +328,11 @@ def main():
         result["fp16_decode_gbs"] = round(fbytes / (f_us * 1e-6) / 1e9, 2)
         result["speedup_vs_fp16_decode"] = round(f_us / dec_med, 3)
         del k16, v16
+
+    if not args.no_uniform:
+        result["uniform_tq_mse"] = uniform_comparison(bg, synth, torch, cfg, rot_k, rot_v, sig, T, n_extra, q_all, ctxs,
+                                                      max_ctx, ws, args, ctx_mean, dec_med,
+                                                      result.get("fp16_decode_us_median"))
 
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_oracle_baseline(bits, sig, rot_k, rot_v, T, args.cpu_seconds)

@@ -61,7 +61,9 @@ class Setup:
 
 
 def make_setup(seed, n_layers, batch, n_kv, group, capacity, k_budget, v_bits, base, dtype="bf16",
-               n_cal=256):
+               n_cal=256, uniform=False):
+    """uniform=True: every RoPE block at k_budget / 64 bits (the uniform
+    TQ-MSE K layout, one K group) instead of the allocator's widths."""
     cfg = bg.Config(n_layers=n_layers, batch=batch, n_kv_heads=n_kv, group=group, capacity=capacity,
                     k_budget=k_budget, v_bits=v_bits,
                     in_dtype=bg.BGTQ_BF16 if dtype == "bf16" else bg.BGTQ_FP32)
@@ -73,8 +75,11 @@ def make_setup(seed, n_layers, batch, n_kv, group, capacity, k_budget, v_bits, b
             sig[layer, h] = synth.sigma_profile(seed, layer, h)
             qc, kc = synth.calibration(seed, layer, h, n_cal, group, sig[layer, h])
             qc, kc = qc.astype(np.float32), kc.astype(np.float32)
-            bits[layer, h] = bg.blockgtq_allocate(bg.blockgtq_energy_scores(qc, kc), k_budget)[0]
-            bits_o[layer, h] = o.allocate(o.energy_scores(qc, kc), k_budget)
+            if uniform:
+                bits[layer, h] = bits_o[layer, h] = k_budget // 64
+            else:
+                bits[layer, h] = bg.blockgtq_allocate(bg.blockgtq_energy_scores(qc, kc), k_budget)[0]
+                bits_o[layer, h] = o.allocate(o.energy_scores(qc, kc), k_budget)
     rot_k, rot_v = synth.rotations(seed)
     return Setup(cfg, seed, base, dtype, bits, bits_o, sig, rot_k, rot_v)
 

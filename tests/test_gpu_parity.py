@@ -154,6 +154,47 @@ def test_qwen_shaped_layer_prefill_then_decode_steps():
     assert stats.code_ties <= 1e-4 * stats.codes
 
 
+@pytest.mark.parametrize("k_budget,v_bits", [(128, 2), (192, 3), (64, 1), (512, 8)])
+def test_uniform_tq_mse_layout(k_budget, v_bits):
+    """The uniform TQ-MSE K layout (every block at k_budget / 64 bits: one K
+    group of all 128 coordinates, one K radius per row), bf16, a ragged batch
+    of two sequences x 2 KV heads, G = 4: codes and radii bit-exact up to
+    counted ties, attention within 2e-3 of the oracle for several split
+    counts, a one-row and a tile-crossing context included."""
+    bg = bgm()
+    st = P.make_setup(5, 1, 2, 2, 4, 3072, k_budget, v_bits, 5e5, "bf16", uniform=True)
+    assert (st.bits == k_budget // 64).all() and (st.bits_oracle == st.bits).all()
+    layout, cache = build(st)
+    lens = [3000, 1301]
+    allkv = {(b, h): P.keys_values(st, 0, h, 1000 * b, lens[b]) for b in range(2) for h in range(2)}
+    # one prefill call: sequence 1's rows beyond its length are other rows
+    pre = [[(np.concatenate([allkv[b, h][0], allkv[0, h][0][:lens[0] - lens[b]]]),
+             np.concatenate([allkv[b, h][1], allkv[0, h][1][:lens[0] - lens[b]]])) for h in range(2)]
+           for b in range(2)]
+    append(st, layout, cache, 0, pre, [0, 0])
+    stats = P.Stats()
+    rows = {}
+    for b in range(2):
+        for h in range(2):
+            rows[b, h] = P.oracle_rows(st, 0, h, allkv[b, h][0], allkv[b, h][1])
+            assert rows[b, h].knorms.shape[1] == 1
+            check_cache(st, cache, 0, b, h, rows[b, h], lens[b], stats, f"uniform K{k_budget // 64} b{b} h{h}")
+    log("uniform", k_budget, v_bits, "ties", vars(stats))
+    q = np.stack([np.concatenate([synth.cast(synth.queries(5, b, h, 0, 4, 5e5), "bf16") for h in range(2)])
+                  for b in range(2)])
+    for ctxl in ([3000, 1301], [1, 65]):
+        ctx = torch.tensor(ctxl, dtype=torch.int32, device="cuda")
+        for ns in (0, 1, 4):
+            out = bg.blockgtq_decode_attn(st.cfg, layout, 0, to_dev(q, "bf16"), ctx, max(ctxl), cache,
+                                          n_splits=ns).cpu().numpy().astype(np.float64)
+            for b in range(2):
+                for h in range(2):
+                    ref = P.oracle_attention(st, 0, h, q[b, h * 4:(h + 1) * 4], rows[b, h], ctxl[b])
+                    err = P.rel_err(out[b, h * 4:(h + 1) * 4], ref)
+                    assert err <= 2e-3, (k_budget, v_bits, ctxl, ns, b, h, err)
+    assert stats.code_ties <= 1e-4 * stats.codes
+
+
 def test_ragged_batch_unaligned_appends_and_edge_lengths():
     """Batch of 4 with different lengths, appends at positions that are not
     tile-aligned (value tiles are read-modify-written), a zero-length context,
