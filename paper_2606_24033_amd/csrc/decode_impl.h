@@ -890,20 +890,39 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   const int nslot = (ng + 1) & ~1;  // radius slots per token
   const RowPtrs R{c.k_codes + row * cap * kw, c.k_norms + row * kMaxGroups * cap,
                   c.v_codes + row * (cap / kTile) * kHeadDim * BV, c.v_norms + row * cap};
-  // the next tile's keys are in flight while a tile is computed; its values
-  // are loaded when it starts and used after its QK products
+  // The next tile's keys are in flight while a tile is computed.  Its values
+  // are too where the registers allow (one query set, rows of <= 8 words,
+  // b_V <= 2);
+  // otherwise a tile's values are loaded when it starts and used after its
+  // QK products.
+  constexpr bool kValuesAhead = NSET == 1 && KWB <= 8 && BV <= 2;
   uint32_t rw[KWB + kRowPad], knp[4], rw2[KWB], knp2[4], vw[4][pv_words<BV>()];
-  uint2 vn;
+  uint32_t vw2[kValuesAhead ? 4 : 1][kValuesAhead ? pv_words<BV>() : 1];
+  uint2 vn, vn2;
 #pragma unroll
   for (int i = KWB; i < KWB + kRowPad; ++i) rw[i] = 0u;
-  if (t0 < t_end) load_keys<KWB>(rw2, knp2, nslot, R, kw, t0, lane);
+  if (t0 < t_end) {
+    load_keys<KWB>(rw2, knp2, nslot, R, kw, t0, lane);
+    if constexpr (kValuesAhead) load_values<BV>(vn2, vw2, R, t0, lane);
+  }
   for (; t0 < t_end; t0 += stride) {
 #pragma unroll
     for (int i = 0; i < KWB; ++i) rw[i] = rw2[i];
 #pragma unroll
     for (int p = 0; p < 4; ++p) knp[p] = knp2[p];
-    load_values<BV>(vn, vw, R, t0, lane);
-    if (t0 + stride < t_end) load_keys<KWB>(rw2, knp2, nslot, R, kw, t0 + stride, lane);
+    if constexpr (kValuesAhead) {
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+#pragma unroll
+        for (int w = 0; w < pv_words<BV>(); ++w) vw[p][w] = vw2[p][w];
+      vn = vn2;
+    } else {
+      load_values<BV>(vn, vw, R, t0, lane);
+    }
+    if (t0 + stride < t_end) {
+      load_keys<KWB>(rw2, knp2, nslot, R, kw, t0 + stride, lane);
+      if constexpr (kValuesAhead) load_values<BV>(vn2, vw2, R, t0 + stride, lane);
+    }
     const int tk = t0 + lane;
     {
       // Re-read the row's width table every tile (scalar loads through an
