@@ -36,7 +36,7 @@
 // 64-bit entry of four fp16 centroids), 2 codes for b = 3, 4, 1 code above.
 // The rotated query is split into fp16 hi and lo parts (both multiplied,
 // accumulated in fp32): fp16 alone leaves ~2^-12 relative error per term.
-// 1-bit groups take the hi part only.
+// 1- and 2-bit groups take the hi part only.
 #pragma once
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
@@ -298,9 +298,10 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
   constexpr int k = 4 * W;
   if constexpr (B == 1) {
     // one 16-byte lookup per code byte: the operands of two steps.  Only the
-    // hi query part: 1-bit blocks are the ones with the least energy, and
-    // leaving out their lo products moves the attention output by ~1e-4
-    // (relative), against ~1e-3 for leaving out every lo product.
+    // hi query part for 1- and 2-bit groups: their blocks are the ones with
+    // the least energy; leaving out their lo products moves the attention
+    // output by <= 3.4e-4 (relative; <= 7.6e-5 for 1-bit groups alone),
+    // against ~9.4e-4 for leaving out every lo product.
     constexpr int by = k / 2;  // byte of step k
     const uint4 u01 = *reinterpret_cast<const uint4*>(smem + (field_at<8 * by, 8, 7>(aw) | rep.r1b));
     const uint4 u23 = *reinterpret_cast<const uint4*>(smem + (field_at<8 * (by + 1), 8, 7>(aw) | rep.r1b));
@@ -324,12 +325,13 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
     // trip per window): without this the compiler sinks each lookup into
     // the branch that uses it and serialises them
     asm volatile("" : "+v"(kv0), "+v"(kv1), "+v"(kv2), "+v"(kv3));
-    qk_mac<NSET, K0 + k, true, Z>(kv0, qh, ql, acc);
+    constexpr bool LO = B != 2;  // hi part only for 2-bit groups (see above)
+    qk_mac<NSET, K0 + k, LO, Z>(kv0, qh, ql, acc);
     if (mm > k + 1) {
-      qk_mac<NSET, K0 + k + 1>(kv1, qh, ql, acc);
+      qk_mac<NSET, K0 + k + 1, LO>(kv1, qh, ql, acc);
       if (mm > k + 2) {
-        qk_mac<NSET, K0 + k + 2>(kv2, qh, ql, acc);
-        if (mm > k + 3) qk_mac<NSET, K0 + k + 3>(kv3, qh, ql, acc);
+        qk_mac<NSET, K0 + k + 2, LO>(kv2, qh, ql, acc);
+        if (mm > k + 3) qk_mac<NSET, K0 + k + 3, LO>(kv3, qh, ql, acc);
       }
     }
   } else {
