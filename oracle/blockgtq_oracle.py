@@ -429,6 +429,19 @@ def attention_rotated(q, key_codes, key_norms, bits, rot_k, val_codes, val_norms
     return acc @ np.asarray(rot_v, dtype=np.float64)
 
 
+def prefill_attention(q: np.ndarray, q_pos, k_hat: np.ndarray, v_hat: np.ndarray) -> np.ndarray:
+    """Causal prefill attention over the cache (Sec. 4, prefill paragraph):
+    query row i sits at absolute position q_pos[i] and attends cache rows
+    0 .. q_pos[i] (inclusive).  q [n, d], k_hat/v_hat [T, d] with T > max(q_pos)
+    -> out [n, d].  Definition mode: one masked softmax per row."""
+    q = np.asarray(q, dtype=np.float64)
+    pos = np.asarray(q_pos, dtype=np.int64)
+    out = np.zeros(q.shape)
+    for i in range(q.shape[0]):   # rows past pos are never read
+        out[i] = attention(q[i:i + 1], k_hat[:pos[i] + 1], v_hat[:pos[i] + 1])[0]
+    return out
+
+
 def attention_partial(q, k_hat, v_hat):
     """(m, l, acc) of one key range: running max, sum of exp, unnormalised output."""
     q = np.asarray(q, dtype=np.float64)

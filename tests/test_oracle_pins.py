@@ -349,6 +349,29 @@ def test_attention_degenerate_cases_and_split_merge():
         np.testing.assert_allclose(o.lse_merge(parts), full, rtol=1e-12, atol=1e-14)
 
 
+def test_prefill_attention_causal_pins():
+    """Causal prefill attention (Sec. 4, prefill paragraph): brute force per
+    row over the keys 0..pos only; position 0 returns value row 0 exactly;
+    equal keys give the running mean of the values; rows past pos never
+    matter (a poisoned tail changes nothing)."""
+    q, bits, rot_k, rot_v, kc, kn, vc, vn = _tiny_cache(seed=5, T=41)
+    kh = o.dequantize_keys(kc, kn, bits, rot_k)
+    vh = o.dequantize_values(vc, vn, rot_v, 2)
+    pos = np.array([0, 3, 17, 40])
+    out = o.prefill_attention(q, pos, kh, vh)
+    for j in range(4):
+        ref = _brute_attention(list(q[j]), kh[:pos[j] + 1].tolist(), vh[:pos[j] + 1].tolist())
+        np.testing.assert_allclose(out[j], ref, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(out[0], vh[0], rtol=1e-13, atol=1e-15)
+    same = np.repeat(kh[:1], 41, 0)
+    want = np.stack([vh[:p + 1].mean(0) for p in pos])
+    np.testing.assert_allclose(o.prefill_attention(q, pos, same, vh), want, rtol=1e-12, atol=1e-14)
+    k2, v2 = kh.copy(), vh.copy()
+    k2[18:] = 1e3
+    v2[18:] = np.nan
+    np.testing.assert_array_equal(o.prefill_attention(q[:3], pos[:3], k2, v2), out[:3])
+
+
 def test_blockgtq_beats_uniform_logit_mae_direction():
     """Trend of the per-layer RoPE-logit MAE comparison (Table 1): on the
     synthetic outlier profile, Block-GTQ's allocation gives lower key logit MAE
