@@ -201,6 +201,30 @@ int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void*
                               void* d_workspace, size_t ws_bytes, int32_t n_splits,
                               void* stream);
 
+/* ---- (f1) prefill attention over the packed cache -----------------------
+ * Causal attention of a prompt's queries over the packed cache of one layer
+ * (Sec. 4, prefill paragraph): query i of sequence b sits at absolute position
+ * d_q_pos0[b] + i and attends cache rows 0 .. that position, which must have
+ * been appended before (blockgtq_quantize_append of the prompt's K/V).  Each
+ * workgroup owns 64 query rows (position x head), decodes every packed key /
+ * value tile of its range once into LDS for all of them, and runs QK^T and PV
+ * on MFMAs under a causal mask and an online softmax; nothing fp16 is written
+ * to HBM.  Async on `stream`; no allocation.
+ * layer: 0 .. n_layers-1 (one layer per call).
+ * d_q: post-RoPE [batch][n_q][n_kv_heads*group][128] in in_dtype, 4-byte
+ *      aligned.  d_out: float, same shape.
+ * d_q_pos0: device int32 [batch].  max_pos (host): an upper bound of every
+ *      d_q_pos0[b] + n_q - 1, below capacity (ECAPACITY otherwise); positions
+ *      are clamped into [0, max_pos] on the device, so every read stays
+ *      inside the cache.
+ * d_workspace / ws_bytes: blockgtq_prefill_workspace_bytes (the rotated
+ *      queries, batch x n_q x n_kv_heads*group x 128 floats); any contents. */
+int blockgtq_prefill_workspace_bytes(const bgtq_config* cfg, int32_t n_q, size_t* bytes_out);
+int blockgtq_prefill_attn(const bgtq_config* cfg, const void* d_layout, int32_t layer,
+                          const void* d_q, int32_t n_q, const int32_t* d_q_pos0, int32_t max_pos,
+                          const bgtq_cache* cache, float* d_out, void* d_workspace,
+                          size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,7 +24,7 @@ EXPORTED = [
     "blockgtq_last_error", "blockgtq_energy_scores", "blockgtq_allocate", "blockgtq_codebook",
     "blockgtq_layout_bytes", "blockgtq_cache_bytes", "blockgtq_workspace_bytes",
     "blockgtq_layout_init", "blockgtq_quantize_append", "blockgtq_decode_attn",
-    "blockgtq_decode_attn_fp16",
+    "blockgtq_decode_attn_fp16", "blockgtq_prefill_workspace_bytes", "blockgtq_prefill_attn",
 ]
 
 
@@ -69,6 +69,8 @@ def lib():
             "blockgtq_quantize_append": [P, P, I32, P, P, I32, P, P, P],
             "blockgtq_decode_attn": [P, P, I32, P, P, I32, P, P, P, SZ, I32, P],
             "blockgtq_decode_attn_fp16": [P, I32, P, P, I32, P, P, P, P, SZ, I32, P],
+            "blockgtq_prefill_workspace_bytes": [P, I32, PSZ],
+            "blockgtq_prefill_attn": [P, P, I32, P, I32, P, I32, P, P, P, SZ, P],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -260,4 +262,29 @@ def blockgtq_decode_attn_fp16(cfg: Config, layer: int, q, ctx_len, max_ctx: int,
     _check(lib().blockgtq_decode_attn_fp16(ctypes.byref(cfg.c()), layer, _ptr(q), _ptr(ctx_len), max_ctx,
                                            _ptr(k16), _ptr(v16), _ptr(out), _ptr(workspace), workspace.numel(),
                                            n_splits, _stream(stream)))
+    return out
+
+
+def prefill_workspace_bytes(cfg: Config, n_q: int) -> int:
+    v = ctypes.c_size_t()
+    _check(lib().blockgtq_prefill_workspace_bytes(ctypes.byref(cfg.c()), n_q, ctypes.byref(v)))
+    return v.value
+
+
+def blockgtq_prefill_attn(cfg: Config, layout: Layout, layer: int, q, q_pos0, max_pos: int, cache: Cache,
+                          out=None, workspace=None, stream=None):
+    """Causal prefill attention of one layer.  q: [batch, n_q, Hq, 128] in the
+    config's input dtype; q_pos0: int32 device tensor [batch] (position of
+    query 0 of each sequence); max_pos: host bound of q_pos0 + n_q - 1."""
+    import torch
+    _check_dev(q, _in_dtype(cfg))
+    _check_dev(q_pos0, torch.int32)
+    n_q = q.shape[1]
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(max(prefill_workspace_bytes(cfg, n_q), 1), dtype=torch.uint8, device=q.device)
+    _check(lib().blockgtq_prefill_attn(ctypes.byref(cfg.c()), _ptr(layout.blob), layer, _ptr(q), n_q, _ptr(q_pos0),
+                                       max_pos, ctypes.byref(cache.c()), _ptr(out), _ptr(workspace),
+                                       workspace.numel(), _stream(stream)))
     return out

@@ -567,4 +567,36 @@ int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void*
   return ok();
 }
 
+int blockgtq_prefill_workspace_bytes(const bgtq_config* cfg, int32_t n_q, size_t* bytes_out) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!bytes_out) return fail(BGTQ_EINVAL, "NULL pointer");
+  if (n_q < 0) return fail(BGTQ_EINVAL, "n_q %d < 0", n_q);
+  *bytes_out = al256(static_cast<size_t>(cfg->batch) * n_q * cfg->n_kv_heads * cfg->group * kHeadDim * 4);
+  return ok();
+}
+
+int blockgtq_prefill_attn(const bgtq_config* cfg, const void* d_layout, int32_t layer, const void* d_q,
+                          int32_t n_q, const int32_t* d_q_pos0, int32_t max_pos, const bgtq_cache* cache,
+                          float* d_out, void* d_workspace, size_t ws_bytes, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (layer < 0 || layer >= cfg->n_layers) return fail(BGTQ_EINVAL, "layer %d out of range (one layer per call)", layer);
+  if (n_q < 0) return fail(BGTQ_EINVAL, "n_q %d < 0", n_q);
+  if (n_q == 0) return ok();
+  if (!d_layout || !d_q || !d_q_pos0 || !d_out || !d_workspace || !cache || !cache->k_codes || !cache->k_norms ||
+      !cache->v_codes || !cache->v_norms)
+    return fail(BGTQ_EINVAL, "NULL pointer");
+  if (reinterpret_cast<uintptr_t>(d_q) % 4 != 0) return fail(BGTQ_EINVAL, "q must be 4-byte aligned");
+  if (max_pos < 0 || max_pos >= cfg->capacity)
+    return fail(BGTQ_ECAPACITY, "max_pos %d outside [0, capacity)", max_pos);
+  size_t need = 0;
+  blockgtq_prefill_workspace_bytes(cfg, n_q, &need);
+  if (ws_bytes < need) return fail(BGTQ_EWORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  CachePtrs c{static_cast<uint32_t*>(cache->k_codes), static_cast<uint16_t*>(cache->k_norms),
+              static_cast<uint32_t*>(cache->v_codes), static_cast<uint16_t*>(cache->v_norms)};
+  hipError_t e = launch_prefill_attn(dims_of(cfg, layer), d_layout, d_q, n_q, d_q_pos0, max_pos, c,
+                                     static_cast<float*>(d_workspace), d_out, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "prefill_attn launch");
+  return ok();
+}
+
 }  // extern "C"

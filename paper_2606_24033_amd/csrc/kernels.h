@@ -55,4 +55,10 @@ hipError_t launch_decode_fp16(const Dims& d, const void* q, const int32_t* ctx_l
                               const void* k16, const void* v16, float* out,
                               const DecodeWs& ws, hipStream_t s);
 
+// Causal prefill attention over the packed cache of one layer (prefill.hip):
+// the query rotation into qr_ws, then the attention into out.
+hipError_t launch_prefill_attn(const Dims& d, const void* layout, const void* q, int n_q,
+                               const int32_t* q_pos0, int max_pos, const CachePtrs& c, float* qr_ws,
+                               float* out, hipStream_t s);
+
 }  // namespace bgtq

@@ -195,6 +195,58 @@ def test_uniform_tq_mse_layout(k_budget, v_bits):
     assert stats.code_ties <= 1e-4 * stats.codes
 
 
+@pytest.mark.parametrize("case", ["llama_k2v2_bf16_chunked", "qwen_k3v3_fp32", "uniform_k8v8"])
+def test_prefill_attention_over_packed_cache(case):
+    """Causal prefill attention over the packed cache (one layer per call):
+    every query row attends rows 0 .. its position; a batch of two with
+    different start positions (a chunked prefill after 700 cached rows), a
+    query count that leaves a ragged last tile, G = 4 and 8, mixed and
+    uniform K layouts, bf16 and fp32 inputs; against the oracle within 2e-3."""
+    bg = bgm()
+    if case == "llama_k2v2_bf16_chunked":
+        st = P.make_setup(7, 2, 2, 2, 4, 1024, 128, 2, 5e5, "bf16")
+        layer, pos0, n_q = 1, [0, 700], 300
+    elif case == "qwen_k3v3_fp32":
+        st = P.make_setup(8, 1, 1, 2, 8, 512, 192, 3, 1e6, "fp32")
+        layer, pos0, n_q = 0, [64], 129
+    else:
+        st = P.make_setup(9, 1, 1, 1, 4, 256, 512, 8, 1e4, "bf16", uniform=True)
+        layer, pos0, n_q = 0, [5], 200
+    B, H, G = st.cfg.batch, st.cfg.n_kv_heads, st.cfg.group
+    layout, cache = build(st)
+    total = [p + n_q for p in pos0]
+    kv = {(b, h): P.keys_values(st, layer, h, 1000 * b, total[b]) for b in range(B) for h in range(H)}
+    T = max(total)
+    pre = []
+    for b in range(B):
+        fill = [P.keys_values(st, layer, h, 5000 + 1000 * b, T - total[b]) for h in range(H)]
+        pre.append([(np.concatenate([kv[b, h][0], fill[h][0]]), np.concatenate([kv[b, h][1], fill[h][1]]))
+                    for h in range(H)])
+    append(st, layout, cache, layer, pre, [0] * B)
+    q = np.stack([np.concatenate([synth.cast(synth.queries(st.seed, 16 * layer + b, h, pos0[b] + i, G, st.base,
+                                                           step=i), st.dtype)[None] for i in range(n_q)])
+                  for b in range(B) for h in range(H)])
+    # q: [B*H, n_q, G, 128] -> [B, n_q, H*G, 128]
+    q = q.reshape(B, H, n_q, G, 128).transpose(0, 2, 1, 3, 4).reshape(B, n_q, H * G, 128)
+    log("prefill", case, "n_q", n_q, "pos0", pos0)
+    qp = torch.tensor(pos0, dtype=torch.int32, device="cuda")
+    out = bg.blockgtq_prefill_attn(st.cfg, layout, layer, to_dev(q, st.dtype), qp, max(total) - 1, cache)
+    out = out.cpu().numpy().astype(np.float64)
+    worst = 0.0
+    for b in range(B):
+        for h in range(H):
+            rows = P.oracle_rows(st, layer, h, kv[b, h][0], kv[b, h][1])
+            kh = o.dequantize_keys(rows.kcodes, rows.knorms, st.bits_oracle[layer, h], st.rot_k)
+            vh = o.dequantize_values(rows.vcodes, rows.vnorms, st.rot_v, st.cfg.v_bits)
+            qq = q[b, :, h * G:(h + 1) * G].reshape(n_q * G, 128)
+            pos = np.repeat(pos0[b] + np.arange(n_q), G)
+            ref = o.prefill_attention(qq, pos, kh, vh).reshape(n_q, G, 128)
+            err = P.rel_err(out[b, :, h * G:(h + 1) * G].reshape(-1, 128), ref.reshape(-1, 128))
+            worst = max(worst, err)
+    log("prefill", case, "max rel err", worst)
+    assert worst <= 2e-3
+
+
 def test_ragged_batch_unaligned_appends_and_edge_lengths():
     """Batch of 4 with different lengths, appends at positions that are not
     tile-aligned (value tiles are read-modify-written), a zero-length context,

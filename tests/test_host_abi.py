@@ -90,3 +90,31 @@ def test_sizes_and_config_errors():
     with pytest.raises(bg.BlockGTQError) as e:
         bg.workspace_bytes(cfg, 32, 0, cfg.capacity + 1)
     assert e.value.code == -3
+
+
+def test_prefill_sizes_and_argument_errors():
+    """Host-side checks of the prefill entry point (rejected before any launch:
+    the pointers are never dereferenced)."""
+    cfg = bg.Config(n_layers=2, batch=3, n_kv_heads=2, group=8, capacity=1024, k_budget=192, v_bits=3)
+    assert bg.prefill_workspace_bytes(cfg, 100) == ((3 * 100 * 16 * 128 * 4 + 255) // 256) * 256
+    assert bg.prefill_workspace_bytes(cfg, 0) == 0
+    with pytest.raises(bg.BlockGTQError) as e:
+        bg.prefill_workspace_bytes(cfg, -1)
+    assert e.value.code == -1
+    L = bg.lib()
+    c = cfg.c()
+    fake = ctypes.c_void_p(256)
+    cache = bg._Cache(256, 256, 256, 256)
+
+    def call(layer=0, n_q=10, max_pos=100, ws=10 ** 9, q=fake):
+        return L.blockgtq_prefill_attn(ctypes.byref(c), fake, layer, q, n_q, fake, max_pos, ctypes.byref(cache),
+                                       fake, fake, ws, None)
+    assert call(layer=-1) == -1            # all-layer calls are decode-only
+    assert call(layer=2) == -1
+    assert call(n_q=-3) == -1
+    assert call(n_q=0) == 0                # nothing to do, nothing launched
+    assert call(max_pos=1024) == -3        # must stay below the capacity
+    assert call(max_pos=-1) == -3
+    assert call(ws=16) == -4
+    assert call(q=ctypes.c_void_p(258)) == -1   # 4-byte alignment
+    assert b"aligned" in L.blockgtq_last_error()
