@@ -9,8 +9,8 @@
 //  1. k_prefill_qrot: the Q-side rotation of every query row into the key
 //     stream order, qr[p] = log2 e (Pi_g q_g)_j / sqrt(d_g d_h) at stream
 //     position p = g_pos[g] + j (fp32, into the caller's workspace);
-//  2. k_prefill_attn: the attention, 64 query rows per workgroup (4 waves of
-//     16 rows).  Decoded key tile: fp32 radius x centroid, stored as fp16 hi
+//  2. k_prefill_attn: the attention, 256 query rows per workgroup (16 waves
+//     of 16 rows), so that each decoded tile serves 256 rows.  Decoded key tile: fp32 radius x centroid, stored as fp16 hi
 //     + lo parts, so that hi/lo query x hi/lo key (three MFMA passes, the
 //     lo x lo product left out) carries ~fp32 precision through one
 //     full-width product per 32 coordinates; the value tile holds the bare
@@ -30,8 +30,9 @@ namespace prefill_detail {
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;  // 4 waves
-constexpr int kRows = 64;      // query rows (position x head) per attention workgroup
+constexpr int kThreads = 256;       // rotation kernel: 4 waves
+constexpr int kAttnThreads = 1024;  // attention kernel: 16 waves of 16 query rows
+constexpr int kRows = 256;          // query rows (position x head) per attention workgroup
 constexpr int kQrotPos = 8;    // query positions per rotation workgroup
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
@@ -46,13 +47,21 @@ constexpr int kOffKRaw = kOffVH + 128 * kVStride * 2;  // [64][k_words] uint32
 constexpr int kOffKNrm = kOffKRaw + 64 * kMaxKWords * 4;  // [64][8] fp16 group radii
 constexpr int kOffVNrm = kOffKNrm + 64 * 8 * 2;           // [64] fp16
 constexpr int kOffCb = kOffVNrm + 64 * 2;                 // fp16 codebooks
-constexpr int kOffMeta = kOffCb + 1024;                   // bitoff u16[128], width u8[128], grp u8[128]
+constexpr int kOffMeta = kOffCb + 1024;                   // per position: bit offset | b << 10 | group << 14 | table << 17
 constexpr int kOffVRaw = kOffMeta + 512;                  // [2 value tiles][128 dims][b_V] uint32
-constexpr int kTileLds = kOffVRaw + 2 * kHeadDim * 8 * 4;
+constexpr int kOffQLo = kOffVRaw + 2 * kHeadDim * 8 * 4;   // [16 waves][4 steps][64 lanes] x 8 fp16: query lo parts
+constexpr int kTileLds = kOffQLo + 16 * 4 * 64 * 16;
 constexpr int kRotVLds = kHeadDim * kHeadDim * 4;         // Pi_V staged for the epilogue
 constexpr int kLdsBytes = kTileLds > kRotVLds ? kTileLds : kRotVLds;
-static_assert(kLdsBytes <= 80 * 1024, "two workgroups per CU");
+static_assert(kLdsBytes <= 160 * 1024, "LDS of one workgroup");
 static_assert(2 * kCodebookEntries <= 1024, "codebook staging");
+
+// Load of a T at a 32-bit byte offset from a wave-uniform base (the global
+// load form with a scalar base and a 32-bit vector offset).
+template <class T>
+__device__ __forceinline__ T ld_at(const void* base, uint32_t byte_off) {
+  return *reinterpret_cast<const T*>(static_cast<const char*>(base) + byte_off);
+}
 
 __device__ __forceinline__ float h2f(uint16_t b) { return static_cast<float>(__builtin_bit_cast(_Float16, b)); }
 
@@ -138,7 +147,7 @@ __global__ __launch_bounds__(kThreads) void k_prefill_qrot(Dims d, const uint8_t
 
 // ---------------------------------------------------------------- 2. attention
 // grid (n_tiles, n_kv, batch), tiles in reverse order (the longest first).
-__global__ __launch_bounds__(kThreads, 2) void k_prefill_attn(Dims d, const uint8_t* __restrict__ blob,
+__global__ __launch_bounds__(kAttnThreads) void k_prefill_attn(Dims d, const uint8_t* __restrict__ blob,
                                                               const float* __restrict__ qr, int n_q,
                                                               const int32_t* __restrict__ q_pos0, int max_pos,
                                                               CachePtrs c, float* __restrict__ out) {
@@ -165,8 +174,10 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill_attn(Dims d, const uint
   const int pos_last = max(0, min(pos0 + i_last, max_pos));
   const int n_kt = pos_last / kKeyTile + 1;
 
-  // query operand (B of S^T = K Q^T): dims 32 ks + 8 g4 .. +7 of the row, hi and lo
-  half8_t qh[4], ql[4];
+  // query operand (B of S^T = K Q^T): dims 32 ks + 8 g4 .. +7 of the row, hi
+  // parts in registers, lo parts in LDS (registers are the limit here)
+  half8_t qh[4];
+  half8_t* qlo = reinterpret_cast<half8_t*>(smem + kOffQLo) + wave * 4 * 64 + lane;
   {
     const float* src = qr + ((static_cast<size_t>(seq) * n_q + min(ri, n_q - 1)) * hq + kvh * G + rh) * kHeadDim;
 #pragma unroll
@@ -174,25 +185,25 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill_attn(Dims d, const uint
       const float4 a = *reinterpret_cast<const float4*>(src + 32 * ks + 8 * g4);
       const float4 b = *reinterpret_cast<const float4*>(src + 32 * ks + 8 * g4 + 4);
       const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      half8_t lo;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float x = valid ? v[e] : 0.f;
         const _Float16 h = static_cast<_Float16>(x);
         qh[ks][e] = h;
-        ql[ks][e] = static_cast<_Float16>(x - static_cast<float>(h));
+        lo[e] = static_cast<_Float16>(x - static_cast<float>(h));
       }
+      qlo[ks * 64] = lo;
     }
   }
   // per-position decode metadata and the codebooks
   uint16_t* cbs = reinterpret_cast<uint16_t*>(smem + kOffCb);
-  uint16_t* mbit = reinterpret_cast<uint16_t*>(smem + kOffMeta);
-  uint8_t* mwid = smem + kOffMeta + 256;
-  uint8_t* mgrp = smem + kOffMeta + 384;
-  for (int i = tid; i < kCodebookEntries; i += kThreads) cbs[i] = c16[i];
+  uint32_t* meta = reinterpret_cast<uint32_t*>(smem + kOffMeta);
+  for (int i = tid; i < kCodebookEntries; i += kAttnThreads) cbs[i] = c16[i];
   if (tid < kHeadDim) {
-    mbit[tid] = M->bitoff[tid];
-    mwid[tid] = M->width[tid];
-    mgrp[tid] = M->grp[tid];
+    const uint32_t b = M->width[tid];
+    meta[tid] = static_cast<uint32_t>(M->bitoff[tid]) | (b << 10) | (static_cast<uint32_t>(M->grp[tid]) << 14) |
+                (static_cast<uint32_t>(cb_index(static_cast<int>(b))) << 17);
   }
 
   const size_t row = (static_cast<size_t>(d.layer) * d.batch + seq) * d.n_kv + kvh;
@@ -213,126 +224,151 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill_attn(Dims d, const uint
 #pragma unroll
   for (int cc = 0; cc < 8; ++cc) o[cc] = float4_t{0.f, 0.f, 0.f, 0.f};
 
+  // Raw words of one tile, one or two per thread (at most 2048 key words,
+  // 2048 value words, 512 key radii, 64 value radii); every load in bounds
+  // (indices clamped), stored only where they exist.
+  const int nk = kKeyTile * kw, nv = 2 * kHeadDim * bv;
+  const int nr_t = tid / nslot;
+  // per-thread byte offsets of the loads (clamped into the tile)
+  const uint32_t ok0 = 4u * min(tid, nk - 1), ok1 = 4u * min(tid + kAttnThreads, nk - 1);
+  const uint32_t ov0 = 4u * min(tid, nv - 1), ov1 = 4u * min(tid + kAttnThreads, nv - 1);
+  const uint32_t okn = 2u * min(tid, kKeyTile * nslot - 1), ovn = 2u * min(tid, kKeyTile - 1);
+  uint32_t pk0, pk1, pv0, pv1;
+  uint16_t pkn, pvn;
+  const auto load_raw = [&](int ta) {
+    const uint32_t* ks = kc + static_cast<size_t>(ta) * kw;
+    const uint32_t* vs = vc + static_cast<size_t>(ta / kTile) * kHeadDim * bv;  // two value tiles, contiguous
+    const uint16_t* ns = kn + static_cast<size_t>(ta) * nslot;
+    // opaque offsets: keeps the scalar-base + 32-bit-offset load form instead
+    // of per-lane 64-bit pointers carried across iterations
+    uint32_t o0 = ok0, o1 = ok1, o2 = ov0, o3 = ov1, o4 = okn, o5 = ovn;
+    asm volatile("" : "+v"(o0), "+v"(o1), "+v"(o2), "+v"(o3), "+v"(o4), "+v"(o5));
+    pk0 = ld_at<uint32_t>(ks, o0);
+    pk1 = ld_at<uint32_t>(ks, o1);
+    pv0 = ld_at<uint32_t>(vs, o2);
+    pv1 = ld_at<uint32_t>(vs, o3);
+    pkn = ld_at<uint16_t>(ns, o4);
+    pvn = ld_at<uint16_t>(vnp + ta, o5);
+  };
+  load_raw(0);
   for (int kt = 0; kt < n_kt; ++kt) {
     const int t0 = kt * kKeyTile;  // t0 + 63 < capacity (a multiple of 64, above pos_last)
     __syncthreads();               // the previous tile's operands are consumed
     // ---- raw tile to LDS: key words and radii, value words and radii
-    for (int i = tid; i < kKeyTile * kw; i += kThreads) kraw[i] = kc[static_cast<size_t>(t0) * kw + i];
-    for (int i = tid; i < 2 * kHeadDim * bv; i += kThreads)  // two 32-token value tiles, contiguous
-      vraw[i] = vc[static_cast<size_t>(t0 / kTile) * kHeadDim * bv + i];
-    for (int i = tid; i < kKeyTile * nslot; i += kThreads) {
-      const int t = i / nslot, gg = i - t * nslot;
-      knrm[t * 8 + gg] = kn[static_cast<size_t>(t0) * nslot + i];
-    }
-    if (tid < kKeyTile) vnrm[tid] = vnp[t0 + tid];
+    // this tile's raw words (loaded during the previous tile) to LDS, then
+    // the next tile's loads, in flight during this tile's decode and products
+    if (tid < nk) kraw[tid] = pk0;
+    if (tid + kAttnThreads < nk) kraw[tid + kAttnThreads] = pk1;
+    if (tid < nv) vraw[tid] = pv0;
+    if (tid + kAttnThreads < nv) vraw[tid + kAttnThreads] = pv1;
+    if (tid < kKeyTile * nslot) knrm[nr_t * 8 + (tid - nr_t * nslot)] = pkn;
+    if (tid < kKeyTile) vnrm[tid] = pvn;
+    if (kt + 1 < n_kt) load_raw(t0 + kKeyTile);
     __syncthreads();
-    // ---- decode the key tile: token t, stream positions 32 pq .. +31
+    // ---- decode the key tile: token t, stream positions pq .. pq + 7
     {
-      const int t = tid >> 2, pq = (tid & 3) * 32;
+      const int t = tid >> 4, pq = (tid & 15) * 8;
       const uint32_t* kr = kraw + t * kw;
-#pragma unroll 4
-      for (int e8 = 0; e8 < 4; ++e8) {
-        half8_t hv, lv;
+      half8_t hv, lv;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int p = pq + 8 * e8 + e;
-          const int off = mbit[p], b = mwid[p], gg = mgrp[p];
-          const int w = off >> 5, sh = off & 31;
-          const uint32_t lo = kr[w];
-          const uint32_t hi = sh + b > 32 ? kr[w + 1] : 0u;
-          const uint32_t code = static_cast<uint32_t>(((static_cast<uint64_t>(hi) << 32) | lo) >> sh) & ((1u << b) - 1u);
-          const float x = h2f(knrm[t * 8 + gg]) * h2f(cbs[cb_index(b) + code]);
-          const _Float16 xh = static_cast<_Float16>(x);
-          hv[e] = xh;
-          lv[e] = static_cast<_Float16>(x - static_cast<float>(xh));
-        }
-        *reinterpret_cast<half8_t*>(khi + t * kKStride + pq + 8 * e8) = hv;
-        *reinterpret_cast<half8_t*>(klo + t * kKStride + pq + 8 * e8) = lv;
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t mt = meta[pq + e];
+        const uint32_t off = mt & 1023u, b = (mt >> 10) & 15u;
+        // the code's word and the next (the next may belong to the next row
+        // or lie past the tile's words: in LDS, and unused then)
+        const uint32_t w = off >> 5;
+        const uint32_t code = __builtin_amdgcn_alignbit(kr[w + 1], kr[w], off & 31u) & ((1u << b) - 1u);
+        const float x = h2f(knrm[t * 8 + ((mt >> 14) & 7u)]) * h2f(cbs[(mt >> 17) + code]);
+        const _Float16 xh = static_cast<_Float16>(x);
+        hv[e] = xh;
+        lv[e] = static_cast<_Float16>(x - static_cast<float>(xh));
       }
+      *reinterpret_cast<half8_t*>(khi + t * kKStride + pq) = hv;
+      *reinterpret_cast<half8_t*>(klo + t * kKStride + pq) = lv;
     }
-    // ---- decode the value tile: dim vd, tokens 32 vhalf .. +31 (codes LSB-first
+    // ---- decode the value tile: dim vd, tokens 8 vq .. 8 vq + 7 (codes LSB-first
     // in the dim's b_V words of its 32-token tile)
     {
-      const int vd = tid >> 1, vhalf = tid & 1;
-      const uint32_t* vr = vraw + (vhalf * kHeadDim + vd) * bv;
+      const int vd = tid >> 3, vq = tid & 7;
+      const uint32_t* vr = vraw + ((vq >> 2) * kHeadDim + vd) * bv;
       const uint16_t* cb = cbs + cb_index(bv);
       const uint32_t mask = (1u << bv) - 1u;
+      half8_t hv;
 #pragma unroll
-      for (int e8 = 0; e8 < 4; ++e8) {
-        half8_t hv;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int bit = (8 * e8 + e) * bv, w = bit >> 5, sh = bit & 31;
-          const uint32_t lo = vr[w];
-          const uint32_t hi = sh + bv > 32 ? vr[w + 1] : 0u;
-          const uint32_t code = static_cast<uint32_t>(((static_cast<uint64_t>(hi) << 32) | lo) >> sh) & mask;
-          hv[e] = __builtin_bit_cast(_Float16, cb[code]);
-        }
-        *reinterpret_cast<half8_t*>(vh + vd * kVStride + 32 * vhalf + 8 * e8) = hv;
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t bit = static_cast<uint32_t>((8 * (vq & 3) + e) * bv);
+        const uint32_t w = bit >> 5;
+        // (the next word may lie past the dim's words: in LDS, and unused then)
+        const uint32_t code = __builtin_amdgcn_alignbit(vr[w + 1], vr[w], bit & 31u) & mask;
+        hv[e] = __builtin_bit_cast(_Float16, cb[code]);
       }
+      *reinterpret_cast<half8_t*>(vh + vd * kVStride + 8 * vq) = hv;
     }
     __syncthreads();
 
-    // ---- S^T = K Q^T: 4 tiles of 16 tokens; lane holds tokens 4 g4 + i of tile j, row l16
-    float4_t s[4];
+    // Two 32-token halves, each: S^T = K Q^T over 2 tiles of 16 tokens (lane
+    // holds tokens 4 g4 + i of tile j, row l16), the causal mask and an
+    // online-softmax update (base 2; one row per lane column), then
+    // O^T += V^T P^T over 8 tiles of 16 dims (lane holds dims 4 g4 + i of
+    // tile cc, row l16).
+#pragma unroll 1
+    for (int hh = 0; hh < 2; ++hh) {
+      float4_t s[2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float4_t acc = {0.f, 0.f, 0.f, 0.f};
-      const int kbase = (16 * j + l16) * kKStride + 8 * g4;
+      for (int jj = 0; jj < 2; ++jj) {
+        float4_t acc = {0.f, 0.f, 0.f, 0.f};
+        const int kbase = (32 * hh + 16 * jj + l16) * kKStride + 8 * g4;
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const half8_t ah = *reinterpret_cast<const half8_t*>(khi + kbase + 32 * ks);
-        const half8_t al = *reinterpret_cast<const half8_t*>(klo + kbase + 32 * ks);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, qh[ks], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, qh[ks], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, ql[ks], acc, 0, 0, 0);
+        for (int ks = 0; ks < 4; ++ks) {
+          const half8_t ah = *reinterpret_cast<const half8_t*>(khi + kbase + 32 * ks);
+          const half8_t al = *reinterpret_cast<const half8_t*>(klo + kbase + 32 * ks);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, qh[ks], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, qh[ks], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, qlo[ks * 64], acc, 0, 0, 0);
+        }
+        s[jj] = acc;
       }
-      s[j] = acc;
-    }
-    // ---- causal mask and online softmax (base 2; one row per lane column)
-    float mx = kNegInf;
+      float mx = kNegInf;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+      for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tok = t0 + 16 * j + 4 * g4 + i;
-        s[j][i] = tok > pos ? kNegInf : s[j][i];
-        mx = fmaxf(mx, s[j][i]);
+        for (int i = 0; i < 4; ++i) {
+          const int tok = t0 + 32 * hh + 16 * jj + 4 * g4 + i;
+          s[jj][i] = tok > pos ? kNegInf : s[jj][i];
+          mx = fmaxf(mx, s[jj][i]);
+        }
+      mx = max4g(mx);
+      // m_run stays -inf only while every token so far is masked (tokens past pos)
+      const float mn = fmaxf(m_run, mx);
+      const float corr = m_run == kNegInf ? 0.f : exp2f(m_run - mn);
+      const float mref = mn == kNegInf ? 0.f : mn;
+      m_run = mn;
+      float ps = 0.f;
+      half8_t pb;  // B operand of O^T = V^T P^T: tokens {4 g4 + i, 16 + 4 g4 + i} of the half
+      {
+        const uint2 va = *reinterpret_cast<const uint2*>(vnrm + 32 * hh + 4 * g4);
+        const uint2 vb = *reinterpret_cast<const uint2*>(vnrm + 32 * hh + 16 + 4 * g4);
+        const uint32_t vr[4] = {va.x, va.y, vb.x, vb.y};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float p = exp2f(s[e >> 2][e & 3] - mref);
+          ps += p;
+          const uint16_t nb = static_cast<uint16_t>(vr[e >> 1] >> (16 * (e & 1)));
+          pb[e] = static_cast<_Float16>(p * h2f(nb));
+        }
       }
-    mx = max4g(mx);
-    const float mn = fmaxf(m_run, mx);  // finite from the first tile on (token 0 <= pos)
-    const float corr = m_run == kNegInf ? 0.f : exp2f(m_run - mn);
-    m_run = mn;
-    float ps = 0.f;
-    half8_t pb[2];  // B operand of O^T = V^T P^T: tokens {4 g4 + i, 16 + 4 g4 + i} of each 32-token step
+      l_run = l_run * corr + ps;
+      if (corr != 1.f) {
 #pragma unroll
-    for (int sstep = 0; sstep < 2; ++sstep) {
-      const uint2 va = *reinterpret_cast<const uint2*>(vnrm + 32 * sstep + 4 * g4);
-      const uint2 vb = *reinterpret_cast<const uint2*>(vnrm + 32 * sstep + 16 + 4 * g4);
-      const uint32_t vr[4] = {va.x, va.y, vb.x, vb.y};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float p = exp2f(s[2 * sstep + (e >> 2)][e & 3] - mn);
-        ps += p;
-        const uint16_t nb = static_cast<uint16_t>(vr[e >> 1] >> (16 * (e & 1)));
-        pb[sstep][e] = static_cast<_Float16>(p * h2f(nb));
+        for (int cc = 0; cc < 8; ++cc) o[cc] *= corr;
       }
-    }
-    l_run = l_run * corr + ps;
-    if (corr != 1.f) {
 #pragma unroll
-      for (int cc = 0; cc < 8; ++cc) o[cc] *= corr;
-    }
-    // ---- O^T += V^T P^T: 8 tiles of 16 dims; lane holds dims 4 g4 + i of tile cc, row l16
-#pragma unroll
-    for (int cc = 0; cc < 8; ++cc) {
-      const _Float16* vrow = vh + (16 * cc + l16) * kVStride + 4 * g4;
-#pragma unroll
-      for (int sstep = 0; sstep < 2; ++sstep) {
-        const uint2 a0 = *reinterpret_cast<const uint2*>(vrow + 32 * sstep);
-        const uint2 a1 = *reinterpret_cast<const uint2*>(vrow + 32 * sstep + 16);
+      for (int cc = 0; cc < 8; ++cc) {
+        const _Float16* vrow = vh + (16 * cc + l16) * kVStride + 32 * hh + 4 * g4;
+        const uint2 a0 = *reinterpret_cast<const uint2*>(vrow);
+        const uint2 a1 = *reinterpret_cast<const uint2*>(vrow + 16);
         const uint4 u = make_uint4(a0.x, a0.y, a1.x, a1.y);
-        o[cc] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, u), pb[sstep], o[cc], 0, 0, 0);
+        o[cc] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, u), pb, o[cc], 0, 0, 0);
       }
     }
   }
@@ -347,7 +383,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill_attn(Dims d, const uint
   float* rv = reinterpret_cast<float*>(smem);
   {
     const float4* src = reinterpret_cast<const float4*>(blob + kOffRotV);
-    for (int i = tid; i < kHeadDim * kHeadDim / 4; i += kThreads) reinterpret_cast<float4*>(rv)[i] = src[i];
+    for (int i = tid; i < kHeadDim * kHeadDim / 4; i += kAttnThreads) reinterpret_cast<float4*>(rv)[i] = src[i];
   }
   __syncthreads();
   float* dst = out + ((static_cast<size_t>(seq) * n_q + min(ri, n_q - 1)) * hq + kvh * G + rh) * kHeadDim;
@@ -379,7 +415,7 @@ hipError_t launch_prefill_attn(const Dims& d, const void* layout, const void* q,
   if (e != hipSuccess) return e;
   const int n_tiles = (n_q * d.group + kRows - 1) / kRows;
   dim3 g2(n_tiles, d.n_kv, d.batch);
-  hipLaunchKernelGGL(k_prefill_attn, g2, dim3(kThreads), 0, s, d, blob, qr_ws, n_q, q_pos0, max_pos, c, out);
+  hipLaunchKernelGGL(k_prefill_attn, g2, dim3(kAttnThreads), 0, s, d, blob, qr_ws, n_q, q_pos0, max_pos, c, out);
   return hipGetLastError();
 }
 
