@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--n-splits", type=int, default=0)
     ap.add_argument("--no-fp16", action="store_true", help="skip the fp16 comparator")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the prefill-attention measurement (one layer, 32K-token prompt)")
+    ap.add_argument("--prefill-len", type=int, default=32768)
     ap.add_argument("--no-uniform", action="store_true",
                     help="skip the uniform TQ-MSE K layout (one K group per head) comparison")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -173,6 +176,58 @@ def uniform_comparison(bg, synth, torch, cfg, rot_k, rot_v, sig, T, n_extra, q_a
     if f16_us is not None:
         res["speedup_vs_fp16_decode"] = round(f16_us / u_us, 3)
     del ucache, ulayout
+    return res
+
+
+def prefill_measurement(bg, synth, torch, bits, sig, rot_k, rot_v, T):
+    """Causal prefill attention over the packed cache for one layer of the same
+    model shape: a T-token prompt quantized into a one-layer cache (layer 0's
+    widths), then blockgtq_prefill_attn for all T query positions.  Timed with
+    HIP events; torch's fp16 causal scaled_dot_product_attention over the same
+    (unquantized) K/V is timed beside it for context."""
+    cfg = bg.Config(n_layers=1, batch=1, n_kv_heads=N_KV, group=GROUP, capacity=((T + 63) // 64) * 64,
+                    k_budget=K_BUDGET, v_bits=V_BITS, in_dtype=bg.BGTQ_BF16)
+    layout = bg.Layout(cfg, bits[:1], synth.flat_rot_k(rot_k), rot_v)
+    cache = bg.Cache(cfg)
+    k, v = synth.torch_layer_kv(SEED, 0, T, sig[0], BASE)
+    bg.blockgtq_quantize_append(cfg, layout, 0, k[None].contiguous(), v[None].contiguous(),
+                                torch.zeros(1, dtype=torch.int32, device="cuda"), cache)
+    q = synth.torch_queries(SEED, 0, N_KV * GROUP, list(range(T)), BASE).reshape(1, T, N_KV * GROUP, 128).contiguous()
+    qp = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out = torch.empty((1, T, N_KV * GROUP, 128), dtype=torch.float32, device="cuda")
+    ws = torch.empty(bg.prefill_workspace_bytes(cfg, T), dtype=torch.uint8, device="cuda")
+
+    def timed(fn, n=5, warm=2):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in ev]))
+
+    ms = timed(lambda: bg.blockgtq_prefill_attn(cfg, layout, 0, q, qp, T - 1, cache, out=out, workspace=ws))
+    flops = N_KV * GROUP * (T * (T + 1) / 2) * 2 * (128 + 128)
+    res = {"workload": f"one Llama-3.1-8B-shaped layer (8 KV heads, 32 q heads), {T}-token prompt, causal, K2V2",
+           "ms_per_call": round(ms, 3), "algorithmic_tflops": round(flops / ms / 1e9, 1),
+           "roofline": {"bound": "mfma", "achieved": round(flops / ms / 1e9, 1), "peak": 2500.0, "unit": "TFLOP/s",
+                        "frac": round(flops / ms / 1e9 / 2500.0, 4),
+                        "flops_per_call": flops, "kernel": "k_prefill_qrot + k_prefill_attn"}}
+    try:
+        k16 = k.half().transpose(0, 1)[None].repeat_interleave(GROUP, dim=1).contiguous()
+        v16 = v.half().transpose(0, 1)[None].repeat_interleave(GROUP, dim=1).contiguous()
+        q16 = q.half().transpose(1, 2).contiguous()
+        sdpa = torch.nn.functional.scaled_dot_product_attention
+        ms16 = timed(lambda: sdpa(q16, k16, v16, is_causal=True))
+        res["torch_sdpa_fp16_causal_ms"] = round(ms16, 3)
+        res["packed_over_fp16_time"] = round(ms / ms16, 3)
+        del k16, v16, q16
+    except Exception as e:  # pragma: no cover - comparator only
+        log(f"fp16 SDPA comparator unavailable: {e}")
+    del cache, layout, out, ws, q, k, v
     return res
 
 
@@ -328,6 +383,9 @@ def main():
         result["fp16_decode_gbs"] = round(fbytes / (f_us * 1e-6) / 1e9, 2)
         result["speedup_vs_fp16_decode"] = round(f_us / dec_med, 3)
         del k16, v16
+
+    if not args.no_prefill:
+        result["prefill_attn"] = prefill_measurement(bg, synth, torch, bits, sig, rot_k, rot_v, args.prefill_len)
 
     if not args.no_uniform:
         result["uniform_tq_mse"] = uniform_comparison(bg, synth, torch, cfg, rot_k, rot_v, sig, T, n_extra, q_all, ctxs,
