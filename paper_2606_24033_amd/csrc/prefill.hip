@@ -33,7 +33,8 @@ typedef float float4_t __attribute__((ext_vector_type(4)));
 constexpr int kThreads = 256;       // rotation kernel: 4 waves
 constexpr int kAttnThreads = 1024;  // attention kernel: 16 waves of 16 query rows
 constexpr int kRows = 256;          // query rows (position x head) per attention workgroup
-constexpr int kQrotPos = 8;    // query positions per rotation workgroup
+constexpr int kQrotPos = 8;          // query positions per rotation chunk (staged together)
+constexpr int kQrotChunks = 16;      // chunks per rotation workgroup (one staging of the rotations)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
 
@@ -101,14 +102,14 @@ __device__ __forceinline__ float ld_q(const void* q, size_t i, int in_dtype) {  
 }
 
 // ---------------------------------------------------------------- 1. rotation
-// grid (ceil(n_q / kQrotPos), n_kv, batch).  qr: [batch][n_q][Hq][128] fp32.
+// grid (ceil(n_q / (kQrotPos kQrotChunks)), n_kv, batch).  qr: [batch][n_q][Hq][128] fp32.
 __global__ __launch_bounds__(kThreads) void k_prefill_qrot(Dims d, const uint8_t* __restrict__ blob,
                                                            const void* __restrict__ q, int n_q,
                                                            float* __restrict__ qr) {
   __shared__ float rs[kRowRotFloats];                // the row's group rotations (transposed blocks)
-  __shared__ float qs[kQrotPos * 8 * kHeadDim];      // the queries in stream order
+  __shared__ float qs[(kQrotPos * 8 + 16) * kHeadDim];  // one chunk of queries in stream order (+ rows read, never stored)
   const int tid = threadIdx.x;
-  const int kvh = blockIdx.y, seq = blockIdx.z, i0 = blockIdx.x * kQrotPos;
+  const int kvh = blockIdx.y, seq = blockIdx.z;
   const int G = d.group, hq = d.n_kv * G;
   const int n_rows_blob = d.n_layers * d.n_kv;
   const RowMeta* M = reinterpret_cast<const RowMeta*>(blob + kOffRows) + (d.layer * d.n_kv + kvh);
@@ -118,30 +119,44 @@ __global__ __launch_bounds__(kThreads) void k_prefill_qrot(Dims d, const uint8_t
   int rtot = 0;
   for (int g = 0; g < ng; ++g) rtot += M->g_dim[g] * M->g_dim[g];
   for (int i = tid; i < rtot; i += kThreads) rs[i] = rowrot[i];
-  const int npos = min(kQrotPos, n_q - i0);
-  for (int e = tid; e < npos * G * kHeadDim; e += kThreads) {
-    const int r = e >> 7, p = e & 127;  // r = position-in-block * G + head
-    const int i = i0 + r / G, h = r - (r / G) * G;
-    const size_t src = ((static_cast<size_t>(seq) * n_q + i) * hq + kvh * G + h) * kHeadDim + M->dim[p];
-    qs[e] = ld_q(q, src, d.in_dtype);
-  }
-  __syncthreads();
   const int p = tid & 127;
   const int g = M->grp[p], p0 = M->g_pos[g], dg = M->g_dim[g], j = p - p0;
+  const int dimp = M->dim[p];
   int off = 0;
   for (int e = 0; e < g; ++e) off += M->g_dim[e] * M->g_dim[e];
   const float* rt = rs + off;  // Pi_dg transposed: rt[k dg + j] = Pi[j][k]
   const float scale = kLog2e * rsqrtf(static_cast<float>(dg) * kHeadDim);
-  for (int r = tid >> 7; r < npos * G; r += kThreads / kHeadDim) {
-    const float* qq = qs + r * kHeadDim + p0;
-    float a0 = 0.f, a1 = 0.f;
-    int k = 0;
-    for (; k + 2 <= dg; k += 2) {
-      a0 = fmaf(rt[k * dg + j], qq[k], a0);
-      a1 = fmaf(rt[(k + 1) * dg + j], qq[k + 1], a1);
+  for (int ch = 0; ch < kQrotChunks; ++ch) {
+    const int i0 = (blockIdx.x * kQrotChunks + ch) * kQrotPos;
+    if (i0 >= n_q) break;  // uniform
+    const int npos = min(kQrotPos, n_q - i0);
+    __syncthreads();  // the previous chunk is consumed (and, first, the rotations are staged)
+    for (int r = tid >> 7; r < npos * G; r += kThreads / kHeadDim) {  // r = position-in-chunk * G + head
+      const int i = i0 + r / G, h = r - (r / G) * G;
+      qs[r * kHeadDim + p] = ld_q(q, ((static_cast<size_t>(seq) * n_q + i) * hq + kvh * G + h) * kHeadDim + dimp,
+                                  d.in_dtype);
     }
-    const int i = i0 + r / G, h = r - (r / G) * G;
-    qr[((static_cast<size_t>(seq) * n_q + i) * hq + kvh * G + h) * kHeadDim + p] = (a0 + a1) * scale;
+    __syncthreads();
+    // rows tid >> 7, + 2, + 4, ...: eight at a time, so that one rotation
+    // coefficient feeds eight independent accumulations
+    const int nr = npos * G;
+    for (int r0 = tid >> 7; r0 < nr; r0 += 16) {
+      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      const float* qq = qs + r0 * kHeadDim + p0;  // rows past nr read stale chunk data, never stored
+      for (int k = 0; k < dg; ++k) {
+        const float a = rt[k * dg + j];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc[u] = fmaf(a, qq[2 * u * kHeadDim + k], acc[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int r = r0 + 2 * u;
+        if (r < nr) {
+          const int i = i0 + r / G, h = r - (r / G) * G;
+          qr[((static_cast<size_t>(seq) * n_q + i) * hq + kvh * G + h) * kHeadDim + p] = acc[u] * scale;
+        }
+      }
+    }
   }
 }
 
@@ -409,7 +424,7 @@ hipError_t launch_prefill_attn(const Dims& d, const void* layout, const void* q,
                                float* out, hipStream_t s) {
   using namespace prefill_detail;
   const uint8_t* blob = static_cast<const uint8_t*>(layout);
-  dim3 g1((n_q + kQrotPos - 1) / kQrotPos, d.n_kv, d.batch);
+  dim3 g1((n_q + kQrotPos * kQrotChunks - 1) / (kQrotPos * kQrotChunks), d.n_kv, d.batch);
   hipLaunchKernelGGL(k_prefill_qrot, g1, dim3(kThreads), 0, s, d, blob, q, n_q, qr_ws);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
