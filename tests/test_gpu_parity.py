@@ -195,7 +195,7 @@ def test_uniform_tq_mse_layout(k_budget, v_bits):
     assert stats.code_ties <= 1e-4 * stats.codes
 
 
-@pytest.mark.parametrize("case", ["llama_k2v2_bf16_chunked", "qwen_k3v3_fp32", "uniform_k8v8"])
+@pytest.mark.parametrize("case", ["llama_k2v2_bf16_chunked", "qwen_k3v3_fp32", "uniform_k8v8", "uniform_k2v2"])
 def test_prefill_attention_over_packed_cache(case):
     """Causal prefill attention over the packed cache (one layer per call):
     every query row attends rows 0 .. its position; a batch of two with
@@ -209,9 +209,12 @@ def test_prefill_attention_over_packed_cache(case):
     elif case == "qwen_k3v3_fp32":
         st = P.make_setup(8, 1, 1, 2, 8, 512, 192, 3, 1e6, "fp32")
         layer, pos0, n_q = 0, [64], 129
-    else:
+    elif case == "uniform_k8v8":
         st = P.make_setup(9, 1, 1, 1, 4, 256, 512, 8, 1e4, "bf16", uniform=True)
         layer, pos0, n_q = 0, [5], 200
+    else:  # every step 2-bit: hi x hi products only
+        st = P.make_setup(10, 1, 1, 2, 4, 1024, 128, 2, 5e5, "bf16", uniform=True)
+        layer, pos0, n_q = 0, [0], 1000
     B, H, G = st.cfg.batch, st.cfg.n_kv_heads, st.cfg.group
     layout, cache = build(st)
     total = [p + n_q for p in pos0]
