@@ -427,8 +427,14 @@ int blockgtq_layout_init(const bgtq_config* cfg, const uint8_t* h_k_bits, const 
     M.n_groups = g;
     for (int w = 0, slot = 0; w < g; ++w) {
       const uint32_t nst = static_cast<uint32_t>(M.g_dim[w] + 3) / 4;
+      // bit 23: the group's width is at most 2 and the row also holds codes of
+      // 4 bits or more, so the group's blocks are among the row's
+      // lowest-energy ones (the allocator gave them the fewest bits): the
+      // decode multiplies only the hi part of the query into them
+      const bool hi_only = M.g_bits[w] <= 2 && M.g_bits[g - 1] >= 4;
       M.gm[M.g_bits[w] - 1] = (1u << 31) | static_cast<uint32_t>(M.bitoff[M.g_pos[w]]) | (nst << 10) |
-                              (static_cast<uint32_t>(slot) << 16) | (static_cast<uint32_t>(w) << 20);
+                              (static_cast<uint32_t>(slot) << 16) | (static_cast<uint32_t>(w) << 20) |
+                              (hi_only ? (1u << 23) : 0u);
       slot += static_cast<int>((nst + 15) / 16);
     }
     // decode steps: 4 coordinates of one group per step

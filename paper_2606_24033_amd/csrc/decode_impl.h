@@ -36,7 +36,8 @@
 // 64-bit entry of four fp16 centroids), 2 codes for b = 3, 4, 1 code above.
 // The rotated query is split into fp16 hi and lo parts (both multiplied,
 // accumulated in fp32): fp16 alone leaves ~2^-12 relative error per term.
-// 1- and 2-bit groups take the hi part only.
+// 1- and 2-bit groups of rows that also hold codes of 4 bits or more take
+// the hi part only.
 #pragma once
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
@@ -291,29 +292,26 @@ __device__ __forceinline__ void qk_mac(const half4_t& kv, const half4_t (&qh)[NS
 // the row or its zero padding: a valid table index, whose MFMA is skipped),
 // so the decoded operands need no merge copies; wider codes take four
 // lookups a step and are decoded only when the step exists.
-template <int B, int NSET, int K0, int W, int N, bool Z = false>
+template <int B, int NSET, int K0, int W, int N, bool Z, bool HI>
 __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&aw)[N], int mm, const LaneRep& rep,
                                           const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
                                           float4_t (&acc)[NSET]) {
   constexpr int k = 4 * W;
   if constexpr (B == 1) {
-    // one 16-byte lookup per code byte: the operands of two steps.  Only the
-    // hi query part for 1- and 2-bit groups: their blocks are the ones with
-    // the least energy; leaving out their lo products moves the attention
-    // output by <= 3.4e-4 (relative; <= 7.6e-5 for 1-bit groups alone),
-    // against ~9.4e-4 for leaving out every lo product.
+    // one 16-byte lookup per code byte: the operands of two steps.  HI: the
+    // hi query part only (see qk_group)
     constexpr int by = k / 2;  // byte of step k
     const uint4 u01 = *reinterpret_cast<const uint4*>(smem + (field_at<8 * by, 8, 7>(aw) | rep.r1b));
     const uint4 u23 = *reinterpret_cast<const uint4*>(smem + (field_at<8 * (by + 1), 8, 7>(aw) | rep.r1b));
     half4_t kv0 = as_half4(u01.x, u01.y), kv1 = as_half4(u01.z, u01.w);
     half4_t kv2 = as_half4(u23.x, u23.y), kv3 = as_half4(u23.z, u23.w);
     asm volatile("" : "+v"(kv0), "+v"(kv1), "+v"(kv2), "+v"(kv3));
-    qk_mac<NSET, K0 + k, false, Z>(kv0, qh, ql, acc);
+    qk_mac<NSET, K0 + k, !HI, Z>(kv0, qh, ql, acc);
     if (mm > k + 1) {
-      qk_mac<NSET, K0 + k + 1, false>(kv1, qh, ql, acc);
+      qk_mac<NSET, K0 + k + 1, !HI>(kv1, qh, ql, acc);
       if (mm > k + 2) {
-        qk_mac<NSET, K0 + k + 2, false>(kv2, qh, ql, acc);
-        if (mm > k + 3) qk_mac<NSET, K0 + k + 3, false>(kv3, qh, ql, acc);
+        qk_mac<NSET, K0 + k + 2, !HI>(kv2, qh, ql, acc);
+        if (mm > k + 3) qk_mac<NSET, K0 + k + 3, !HI>(kv3, qh, ql, acc);
       }
     }
   } else if constexpr (B <= 4) {
@@ -325,7 +323,7 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
     // trip per window): without this the compiler sinks each lookup into
     // the branch that uses it and serialises them
     asm volatile("" : "+v"(kv0), "+v"(kv1), "+v"(kv2), "+v"(kv3));
-    constexpr bool LO = B != 2;  // hi part only for 2-bit groups (see above)
+    constexpr bool LO = !HI;
     qk_mac<NSET, K0 + k, LO, Z>(kv0, qh, ql, acc);
     if (mm > k + 1) {
       qk_mac<NSET, K0 + k + 1, LO>(kv1, qh, ql, acc);
@@ -348,7 +346,7 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
 
 // Sub-chunk SC of a 16-step slot: realign its bits (stream bit ob onwards)
 // to bit 0 of aw, then run its min(CH, ms - SC CH) steps.
-template <int B, int NSET, int KWB, bool Z, int SC>
+template <int B, int NSET, int KWB, bool Z, bool HI, int SC>
 __device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t (&rw)[KWB + kRowPad], int ob, int ms,
                                              const LaneRep& rep, const half4_t (&qh)[NSET],
                                              const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
@@ -362,23 +360,29 @@ __device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t
     for (int i = 0; i < NW; ++i) aw[i] = __builtin_amdgcn_alignbit(rw[w0 + i + 1], rw[w0 + i], sh);
     aw[NW] = 0;
     const int mm = min(CH, ms - SC * CH);
-    qk_window<B, NSET, SC * CH, 0, NW + 1, Z && SC == 0>(smem, aw, mm, rep, qh, ql, acc);
+    qk_window<B, NSET, SC * CH, 0, NW + 1, Z && SC == 0, HI>(smem, aw, mm, rep, qh, ql, acc);
     if constexpr (CH == 8) {
-      if (mm > 4) qk_window<B, NSET, SC * CH, 1, NW + 1>(smem, aw, mm, rep, qh, ql, acc);
+      if (mm > 4) qk_window<B, NSET, SC * CH, 1, NW + 1, false, HI>(smem, aw, mm, rep, qh, ql, acc);
     }
   }
 }
 
-template <int B, int NSET, int KWB, bool Z, int... SC>
+template <int B, int NSET, int KWB, bool Z, bool HI, int... SC>
 __device__ __forceinline__ void qk_slot(std::integer_sequence<int, SC...>, const uint8_t* smem,
                                         const uint32_t (&rw)[KWB + kRowPad], int ob, int ms, const LaneRep& rep,
                                         const half4_t (&qh)[NSET], const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
-  (qk_slot_part<B, NSET, KWB, Z, SC>(smem, rw, ob, ms, rep, qh, ql, acc), ...);
+  (qk_slot_part<B, NSET, KWB, Z, HI, SC>(smem, rw, ob, ms, rep, qh, ql, acc), ...);
 }
 
 // The group of width B (metadata gm, radius bits nrm16 of the lane's token):
-// L += radius * <rotated query, dequantized unit-norm codes>.
-template <int B, int NSET, int KWB>
+// L += radius * <rotated query, dequantized unit-norm codes>.  HI: the hi
+// part of the query only, for groups of width <= 2 in rows that also hold
+// codes of 4 bits or more (the layout's flag): their blocks are among the
+// row's lowest-energy ones, and leaving out their lo products moves the
+// attention output by <= 3.4e-4 (relative) on the Llama-shaped workload.  A
+// row whose low widths carry most of the energy (a uniform 1- or 2-bit
+// layout) keeps both parts: fp16 queries alone cost ~3e-3 there.
+template <int B, int NSET, int KWB, bool HI>
 __device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&rw)[KWB + kRowPad], uint32_t gm,
                                          uint32_t nrm16, const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
   const int o = gm_off(gm), nst = gm_steps(gm), slot0 = gm_slot(gm);
@@ -393,8 +397,8 @@ __device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&r
       qh[s] = as_half4(uh.x, uh.y);
       ql[s] = as_half4(ul.x, ul.y);
     }
-    qk_slot<B, NSET, KWB, decltype(first)::value>(std::make_integer_sequence<int, 16 / qk_ch<B>()>{}, smem, rw,
-                                                  o + 64 * B * c, min(16, nst - 16 * c), rep, qh, ql, acc);
+    qk_slot<B, NSET, KWB, decltype(first)::value, HI>(std::make_integer_sequence<int, 16 / qk_ch<B>()>{}, smem, rw,
+                                                      o + 64 * B * c, min(16, nst - 16 * c), rep, qh, ql, acc);
   };
   slot(std::true_type{}, 0);
   for (int c = 1; c * 16 < nst; ++c) slot(std::false_type{}, c);
@@ -527,8 +531,12 @@ template <int NSET, int KWB, int... BM1>
 __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const uint8_t* smem,
                                        const uint32_t (&rw)[KWB + kRowPad], const uint32_t (&knp)[4],
                                        const uint32_t (&gmb)[8], const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
-  ((gmb[BM1] >> 31 ? qk_group<BM1 + 1, NSET, KWB>(smem, rw, gmb[BM1], radius_bits(knp, gm_plane(gmb[BM1])), rep,
-                                                  lane, L)
+  // (the hi-only variant exists for widths 1 and 2; the flag is uniform)
+  ((gmb[BM1] >> 31 ? (BM1 < 2 && ((gmb[BM1] >> 23) & 1u)
+                          ? qk_group<BM1 + 1, NSET, KWB, BM1 < 2>(smem, rw, gmb[BM1],
+                                                                  radius_bits(knp, gm_plane(gmb[BM1])), rep, lane, L)
+                          : qk_group<BM1 + 1, NSET, KWB, false>(smem, rw, gmb[BM1],
+                                                                radius_bits(knp, gm_plane(gmb[BM1])), rep, lane, L))
                    : void()),
    ...);
 }

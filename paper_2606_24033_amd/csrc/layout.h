@@ -56,7 +56,8 @@ struct RowMeta {
   // packed decode metadata by width b (entry b - 1; 0 = width absent): bit 31
   // present, bits 0..9 first stream bit, 10..15 steps, 16..19 first query
   // slot (16 steps per slot, slots numbered group after group), 20..22 the
-  // group ordinal
+  // group ordinal, 23 hi part of the query only (a width <= 2 group in a row
+  // that also holds codes of 4 bits or more)
   uint32_t gm[8];
   int32_t pad[13];
 };

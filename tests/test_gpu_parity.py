@@ -250,6 +250,32 @@ def test_prefill_attention_over_packed_cache(case):
     assert worst <= 2e-3
 
 
+def test_uniform_k2_decode_many_positions():
+    """Decode over a uniform K2 layout (one 2-bit group holding the whole
+    key), the layout where the dropped lo part of the query matters most:
+    27 contexts from 1 to 989 rows, each with the query of its position,
+    against the oracle within 2e-3."""
+    bg = bgm()
+    st = P.make_setup(10, 1, 1, 2, 4, 1024, 128, 2, 5e5, "bf16", uniform=True)
+    layout, cache = build(st)
+    T = 1000
+    kv = [P.keys_values(st, 0, h, 0, T) for h in range(2)]
+    append(st, layout, cache, 0, [[kv[h] for h in range(2)]], [0])
+    rows = [P.oracle_rows(st, 0, h, kv[h][0], kv[h][1]) for h in range(2)]
+    worst = 0.0
+    for ctx_n in range(1, T, 37):
+        q = np.concatenate([synth.cast(synth.queries(10, 0, h, ctx_n - 1, 4, 5e5, step=ctx_n), "bf16")
+                            for h in range(2)])
+        ctx = torch.tensor([ctx_n], dtype=torch.int32, device="cuda")
+        out = bg.blockgtq_decode_attn(st.cfg, layout, 0, to_dev(q[None], "bf16"), ctx, ctx_n, cache)
+        out = out[0].cpu().numpy().astype(np.float64)
+        for h in range(2):
+            ref = P.oracle_attention(st, 0, h, q[h * 4:(h + 1) * 4], rows[h], ctx_n)
+            worst = max(worst, P.rel_err(out[h * 4:(h + 1) * 4], ref))
+    log("uniform K2 decode, max rel err", worst)
+    assert worst <= 2e-3
+
+
 def test_ragged_batch_unaligned_appends_and_edge_lengths():
     """Batch of 4 with different lengths, appends at positions that are not
     tile-aligned (value tiles are read-modify-written), a zero-length context,
