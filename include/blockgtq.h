@@ -206,7 +206,7 @@ int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void*
  * (Sec. 4, prefill paragraph): query i of sequence b sits at absolute position
  * d_q_pos0[b] + i and attends cache rows 0 .. that position, which must have
  * been appended before (blockgtq_quantize_append of the prompt's K/V).  Each
- * workgroup owns 64 query rows (position x head), decodes every packed key /
+ * workgroup owns 256 query rows (position x head), decodes every packed key /
  * value tile of its range once into LDS for all of them, and runs QK^T and PV
  * on MFMAs under a causal mask and an online softmax; nothing fp16 is written
  * to HBM.  Async on `stream`; no allocation.
@@ -224,6 +224,52 @@ int blockgtq_prefill_attn(const bgtq_config* cfg, const void* d_layout, int32_t 
                           const void* d_q, int32_t n_q, const int32_t* d_q_pos0, int32_t max_pos,
                           const bgtq_cache* cache, float* d_out, void* d_workspace,
                           size_t ws_bytes, void* stream);
+
+/* ---- (f4) protected fp16 window ------------------------------------------
+ * The "protected" regime of the reasoning evaluation (Sec. 6, AIME paragraph,
+ * and the buffer configurations of its appendix): during decode the cache of
+ * a sequence with T rows reads as [sink | packed | recent], where the first
+ * n_s = min(n_sink, T) rows and the last n_r = min(n_recent, T - n_s) rows
+ * are kept in fp16 and the rows in between come from the packed cache (the
+ * paper's setting is n_sink = 4, n_recent = 128; 0 and 0 is the no-buffer
+ * regime).  The packed cache still receives every row
+ * (blockgtq_quantize_append); the window is a second, caller-owned store.
+ *
+ * d_window: fp16 [n_layers][batch][n_kv_heads][2][n_sink + n_recent][128],
+ *   keys then values; position t < n_sink lives in slot t, a later position
+ *   in slot n_sink + (t - n_sink) mod n_recent (a ring).
+ * n_sink in 0..63 (the sink ends inside the first 64-row tile of the packed
+ * pass), n_recent in 0..1024; EINVAL otherwise.  With both 0 the window is
+ * empty and d_window may be NULL. */
+int blockgtq_window_bytes(const bgtq_config* cfg, int32_t n_sink, int32_t n_recent, size_t* bytes_out);
+
+/* Writes the fp16 copies of appended rows into the window (async on
+ * `stream`).  Arguments as blockgtq_quantize_append (same d_k / d_v layouts
+ * and positions); a row at position t is written if t < n_sink or if it is
+ * one of the call's last n_recent rows, so a chunk longer than the recent
+ * window leaves exactly its last n_recent rows in the ring.  Call it for
+ * every row that blockgtq_quantize_append receives. */
+int blockgtq_window_append(const bgtq_config* cfg, int32_t layer, const void* d_k, const void* d_v, int32_t n_new,
+                           const int32_t* d_write_pos, int32_t n_sink, int32_t n_recent, void* d_window,
+                           void* stream);
+
+/* Workspace of blockgtq_decode_attn_protected: blockgtq_workspace_bytes plus
+ * the window's partials ([n_layers_in_call][batch][n_kv_heads*group][130]
+ * floats).  The counters at its start follow the same rules (zero-filled once
+ * before first use; every completed call leaves them zero). */
+int blockgtq_protected_workspace_bytes(const bgtq_config* cfg, int32_t n_layers_in_call, int32_t n_splits,
+                                       int32_t max_ctx, size_t* bytes_out);
+
+/* Decode attention over [sink | packed | recent]: arguments as
+ * blockgtq_decode_attn, plus the window.  Two launches on `stream`: the
+ * window kernel (exact fp32 logits and weights over the fp16 rows, its
+ * partial written into the workspace), then the packed decode over rows
+ * [n_s, T - n_r) whose merge adds the window's partial by log-sum-exp.  A
+ * context that the window covers (T <= n_s + n_r) reads no packed rows. */
+int blockgtq_decode_attn_protected(const bgtq_config* cfg, const void* d_layout, int32_t layer, const void* d_q,
+                                   const int32_t* d_ctx_len, int32_t max_ctx, const bgtq_cache* cache,
+                                   const void* d_window, int32_t n_sink, int32_t n_recent, float* d_out,
+                                   void* d_workspace, size_t ws_bytes, int32_t n_splits, void* stream);
 
 #ifdef __cplusplus
 }

@@ -442,6 +442,26 @@ def prefill_attention(q: np.ndarray, q_pos, k_hat: np.ndarray, v_hat: np.ndarray
     return out
 
 
+def protected_attention(q: np.ndarray, k_hat: np.ndarray, v_hat: np.ndarray, k16: np.ndarray, v16: np.ndarray,
+                        n_sink: int, n_recent: int) -> np.ndarray:
+    """Decode attention in the protected-buffer regime (Sec. 6, reasoning
+    evaluation, and the buffer configurations of its appendix): of a context
+    of T rows, the first n_s = min(n_sink, T) and the last
+    n_r = min(n_recent, T - n_s) keep their fp16 keys/values (k16, v16,
+    [T, d], already fp16-rounded), the rows in between are the dequantized
+    ones (k_hat, v_hat).  Definition mode: the keys and values of every row
+    are picked, then one softmax over all T rows.  q [Hg, d] -> [Hg, d]."""
+    T = k_hat.shape[0]
+    ns = min(n_sink, T)
+    nr = min(n_recent, T - ns)
+    fp16_row = np.zeros(T, dtype=bool)
+    fp16_row[:ns] = True
+    fp16_row[T - nr:] = True
+    k = np.where(fp16_row[:, None], np.asarray(k16, dtype=np.float64), np.asarray(k_hat, dtype=np.float64))
+    v = np.where(fp16_row[:, None], np.asarray(v16, dtype=np.float64), np.asarray(v_hat, dtype=np.float64))
+    return attention(q, k, v)
+
+
 def attention_partial(q, k_hat, v_hat):
     """(m, l, acc) of one key range: running max, sum of exp, unnormalised output."""
     q = np.asarray(q, dtype=np.float64)

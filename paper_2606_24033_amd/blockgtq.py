@@ -25,6 +25,8 @@ EXPORTED = [
     "blockgtq_layout_bytes", "blockgtq_cache_bytes", "blockgtq_workspace_bytes",
     "blockgtq_layout_init", "blockgtq_quantize_append", "blockgtq_decode_attn",
     "blockgtq_decode_attn_fp16", "blockgtq_prefill_workspace_bytes", "blockgtq_prefill_attn",
+    "blockgtq_window_bytes", "blockgtq_window_append", "blockgtq_protected_workspace_bytes",
+    "blockgtq_decode_attn_protected",
 ]
 
 
@@ -71,6 +73,10 @@ def lib():
             "blockgtq_decode_attn_fp16": [P, I32, P, P, I32, P, P, P, P, SZ, I32, P],
             "blockgtq_prefill_workspace_bytes": [P, I32, PSZ],
             "blockgtq_prefill_attn": [P, P, I32, P, I32, P, I32, P, P, P, SZ, P],
+            "blockgtq_window_bytes": [P, I32, I32, PSZ],
+            "blockgtq_window_append": [P, I32, P, P, I32, P, I32, I32, P, P],
+            "blockgtq_protected_workspace_bytes": [P, I32, I32, I32, PSZ],
+            "blockgtq_decode_attn_protected": [P, P, I32, P, P, I32, P, P, I32, I32, P, P, SZ, I32, P],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -287,4 +293,56 @@ def blockgtq_prefill_attn(cfg: Config, layout: Layout, layer: int, q, q_pos0, ma
     _check(lib().blockgtq_prefill_attn(ctypes.byref(cfg.c()), _ptr(layout.blob), layer, _ptr(q), n_q, _ptr(q_pos0),
                                        max_pos, ctypes.byref(cache.c()), _ptr(out), _ptr(workspace),
                                        workspace.numel(), _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------- protected fp16 window
+
+def window_bytes(cfg: Config, n_sink: int, n_recent: int) -> int:
+    v = ctypes.c_size_t()
+    _check(lib().blockgtq_window_bytes(ctypes.byref(cfg.c()), n_sink, n_recent, ctypes.byref(v)))
+    return v.value
+
+
+def protected_workspace_bytes(cfg: Config, n_layers_in_call: int, n_splits: int, max_ctx: int) -> int:
+    v = ctypes.c_size_t()
+    _check(lib().blockgtq_protected_workspace_bytes(ctypes.byref(cfg.c()), n_layers_in_call, n_splits, max_ctx,
+                                                    ctypes.byref(v)))
+    return v.value
+
+
+def blockgtq_window_append(cfg: Config, layer: int, k, v, write_pos, n_sink: int, n_recent: int, window,
+                           stream=None):
+    """fp16 copies of appended rows into the window (same k, v, write_pos as
+    blockgtq_quantize_append).  window: fp16 device tensor of window_bytes."""
+    import torch
+    for t in (k, v):
+        _check_dev(t, _in_dtype(cfg))
+    _check_dev(write_pos, torch.int32)
+    _check_dev(window, torch.float16)
+    if window.numel() * 2 < window_bytes(cfg, n_sink, n_recent):
+        raise BlockGTQError(-1, "window tensor too small")
+    _check(lib().blockgtq_window_append(ctypes.byref(cfg.c()), layer, _ptr(k), _ptr(v), k.shape[-3], _ptr(write_pos),
+                                        n_sink, n_recent, _ptr(window), _stream(stream)))
+
+
+def blockgtq_decode_attn_protected(cfg: Config, layout: Layout, layer: int, q, ctx_len, max_ctx: int, cache: Cache,
+                                   window, n_sink: int, n_recent: int, out=None, workspace=None, n_splits: int = 0,
+                                   stream=None):
+    import torch
+    _check_dev(q, _in_dtype(cfg))
+    _check_dev(ctx_len, torch.int32)
+    _check_dev(window, torch.float16)
+    if window.numel() * 2 < window_bytes(cfg, n_sink, n_recent):
+        raise BlockGTQError(-1, "window tensor too small")
+    n_lc = cfg.n_layers if layer < 0 else 1
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = torch.zeros(protected_workspace_bytes(cfg, n_lc, n_splits, max_ctx), dtype=torch.uint8,
+                                device=q.device)
+    _check(lib().blockgtq_decode_attn_protected(ctypes.byref(cfg.c()), _ptr(layout.blob), layer, _ptr(q),
+                                                _ptr(ctx_len), max_ctx, ctypes.byref(cache.c()), _ptr(window),
+                                                n_sink, n_recent, _ptr(out), _ptr(workspace), workspace.numel(),
+                                                n_splits, _stream(stream)))
     return out

@@ -573,6 +573,78 @@ int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void*
   return ok();
 }
 
+static int check_window(int32_t n_sink, int32_t n_recent) {
+  if (n_sink < 0 || n_sink > kMaxSink) return fail(BGTQ_EINVAL, "n_sink %d outside 0..%d", n_sink, kMaxSink);
+  if (n_recent < 0 || n_recent > kMaxRecent)
+    return fail(BGTQ_EINVAL, "n_recent %d outside 0..%d", n_recent, kMaxRecent);
+  return BGTQ_OK;
+}
+
+int blockgtq_window_bytes(const bgtq_config* cfg, int32_t n_sink, int32_t n_recent, size_t* bytes_out) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!bytes_out) return fail(BGTQ_EINVAL, "NULL pointer");
+  if (int e = check_window(n_sink, n_recent)) return e;
+  *bytes_out = static_cast<size_t>(cfg->n_layers) * cfg->batch * cfg->n_kv_heads * 2 *
+               static_cast<size_t>(n_sink + n_recent) * kHeadDim * 2;
+  return ok();
+}
+
+int blockgtq_window_append(const bgtq_config* cfg, int32_t layer, const void* d_k, const void* d_v, int32_t n_new,
+                           const int32_t* d_write_pos, int32_t n_sink, int32_t n_recent, void* d_window,
+                           void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (int e = check_window(n_sink, n_recent)) return e;
+  if (layer < -1 || layer >= cfg->n_layers) return fail(BGTQ_EINVAL, "layer %d out of range", layer);
+  if (n_new < 0) return fail(BGTQ_EINVAL, "n_new %d < 0", n_new);
+  if (n_new > cfg->capacity) return fail(BGTQ_ECAPACITY, "n_new %d > capacity %d", n_new, cfg->capacity);
+  if (n_new == 0 || n_sink + n_recent == 0) return ok();
+  if (!d_k || !d_v || !d_write_pos || !d_window) return fail(BGTQ_EINVAL, "NULL pointer");
+  hipError_t e = launch_window_append(dims_of(cfg, layer), d_k, d_v, n_new, d_write_pos, n_sink, n_recent,
+                                      static_cast<_Float16*>(d_window), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "window_append launch");
+  return ok();
+}
+
+int blockgtq_protected_workspace_bytes(const bgtq_config* cfg, int32_t n_layers_in_call, int32_t n_splits,
+                                       int32_t max_ctx, size_t* bytes_out) {
+  size_t base = 0;
+  if (int e = blockgtq_workspace_bytes(cfg, n_layers_in_call, n_splits, max_ctx, &base)) return e;
+  *bytes_out = base + al256(static_cast<size_t>(n_layers_in_call) * cfg->batch * cfg->n_kv_heads * cfg->group * 130 * 4);
+  return ok();
+}
+
+int blockgtq_decode_attn_protected(const bgtq_config* cfg, const void* d_layout, int32_t layer, const void* d_q,
+                                   const int32_t* d_ctx_len, int32_t max_ctx, const bgtq_cache* cache,
+                                   const void* d_window, int32_t n_sink, int32_t n_recent, float* d_out,
+                                   void* d_workspace, size_t ws_bytes, int32_t n_splits, void* stream) {
+  DecodeWs ws;
+  if (int e = check_window(n_sink, n_recent)) return e;
+  if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws))
+    return e;
+  if (!d_layout || (!d_window && n_sink + n_recent > 0) || !cache || !cache->k_codes || !cache->k_norms ||
+      !cache->v_codes || !cache->v_norms)
+    return fail(BGTQ_EINVAL, "NULL pointer");
+  const int n_lc = layer < 0 ? cfg->n_layers : 1;
+  size_t need = 0;
+  blockgtq_protected_workspace_bytes(cfg, n_lc, n_splits, max_ctx, &need);
+  if (ws_bytes < need) return fail(BGTQ_EWORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  float* wpart = reinterpret_cast<float*>(static_cast<uint8_t*>(d_workspace) +
+                                          ws_bytes_of(cfg, n_lc, plan_splits(cfg, n_lc, max_ctx, n_splits)));
+  ws.wpart = wpart;
+  ws.n_sink = n_sink;
+  ws.n_recent = n_recent;
+  const Dims d = dims_of(cfg, layer);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_window_attn(d, d_layout, d_q, d_ctx_len, static_cast<const _Float16*>(d_window), n_sink,
+                                    n_recent, wpart, s);
+  if (e != hipSuccess) return hip_fail(e, "window_attn launch");
+  CachePtrs c{static_cast<uint32_t*>(cache->k_codes), static_cast<uint16_t*>(cache->k_norms),
+              static_cast<uint32_t*>(cache->v_codes), static_cast<uint16_t*>(cache->v_norms)};
+  e = launch_decode_packed(d, d_layout, d_q, d_ctx_len, c, d_out, ws, s);
+  if (e != hipSuccess) return hip_fail(e, "decode_attn_protected launch");
+  return ok();
+}
+
 int blockgtq_prefill_workspace_bytes(const bgtq_config* cfg, int32_t n_q, size_t* bytes_out) {
   if (int e = check_cfg(cfg)) return e;
   if (!bytes_out) return fail(BGTQ_EINVAL, "NULL pointer");

@@ -547,12 +547,26 @@ __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const
 // (exact log-sum-exp; it resets the unit's counter), then out = R^T o with R
 // the V rotation (rotv) or none, o scaled by oscale.  The merge area of LDS
 // starts at smem; `last` is a flag word outside it.
+// Log-sum-exp merge of the protected window's partial (m, l, acc[128], written
+// by the window kernel before this launch) into a running (mx, l, a).
+__device__ __forceinline__ void merge_window(const float* __restrict__ w, int dd, float& mx, float& l, float& a) {
+  const float mw = w[0];
+  if (mw == kNegInf) return;
+  const float mc = fmaxf(mx, mw);
+  const float r = mx == kNegInf ? 0.f : exp2_hw(mx - mc);
+  const float e = exp2_hw(mw - mc);
+  l = fmaf(w[1], e, l * r);
+  a = fmaf(w[2 + dd], e, a * r);
+  mx = mc;
+}
+
 template <int NSET>
 __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims& d, int G, int lz, int kvh,
                                             int split, int tid, int lane, int wave, float (&m_run)[NSET],
                                             float (&l_run)[NSET], const float4_t (&O)[NSET][2],
                                             int32_t* __restrict__ counters, float* __restrict__ part, int n_splits,
-                                            float oscale, const float* __restrict__ rotv, float* __restrict__ out) {
+                                            float oscale, const float* __restrict__ rotv, float* __restrict__ out,
+                                            const float* __restrict__ wpart) {
   const int hqn = d.n_kv * G;
   const int bq = lane >> 2, jq = lane & 3;
 #pragma unroll
@@ -591,6 +605,7 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
       }
     }
     if (n_splits == 1) {
+      if (wpart != nullptr) merge_window(wpart + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * 130, dd, mx, l, a);
       os[i] = l > 0.f ? a / l * oscale : 0.f;
     } else {
       // device-coherent stores (no L2 write-back needed before the counter)
@@ -652,6 +667,7 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
         }
         mx = mc;
       }
+      if (wpart != nullptr) merge_window(wpart + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * 130, dd, mx, l, a);
       os[i] = l > 0.f ? a / l * oscale : 0.f;
     }
     if (tid == 0) __hip_atomic_store(counters + lz * d.n_kv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -674,7 +690,7 @@ template <int NSET, int KWB, int BV>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 16 ? 3 : 4))) void k_split_mfma(
     Dims d, const uint8_t* __restrict__ blob, const void* __restrict__ q, const int32_t* __restrict__ ctx_len,
     CachePtrs c, float* __restrict__ out, int32_t* __restrict__ counters, float* __restrict__ part, int n_splits,
-    int split_len) {
+    int split_len, WinArgs win) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: tile addresses stay scalar
@@ -879,8 +895,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   asm volatile("" : "+v"(rep.r1), "+v"(rep.r3), "+v"(rep.r4), "+v"(rep.r5), "+v"(rep.r2), "+v"(rep.r1b));
 
   const int ctx = min(ctx_len[seq], cap);
+  // packed rows [t_lo, t_hi): all of them, or those between the protected
+  // window's sink and recent rows (none when the window covers the context;
+  // t_lo < 64, so the first tile of a non-empty range holds a row of it)
+  int t_lo = 0, t_hi = ctx;
+  if (win.part != nullptr) {
+    const int ns = min(win.n_sink, ctx);
+    t_lo = ns;
+    t_hi = ctx - min(win.n_recent, ctx - ns);
+    if (t_hi <= t_lo) t_lo = t_hi = 0;
+  }
   const int t_begin = split * split_len;
-  const int t_end = min(t_begin + split_len, ctx);
+  const int t_end = min(t_begin + split_len, t_hi);
   const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + kvh;
 
   float m_run[NSET], l_run[NSET];
@@ -955,21 +981,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     // Logits are in base-2 units (log2 e is folded into the query).  Only a
     // tile that reaches past the split end masks anything: its scores past
     // the end become -inf and their value radii 0.
-    const bool full = t0 + 64 <= t_end;
+    const bool full = t0 >= t_lo && t0 + 64 <= t_end;
     // value radii stay packed fp16: p n_V is one mixed-precision product
     // into each half of the PV operand (the codes' 1/sqrt(d_h) scales the
     // output instead)
     uint2 vr = vn;
     if (!full) {
-      const int e = t_end - (t0 + 4 * bq);  // radii of tokens >= e are cleared
-      vr.x &= e <= 0 ? 0u : (e == 1 ? 0xFFFFu : 0xFFFFFFFFu);
-      vr.y &= e <= 2 ? 0u : (e == 3 ? 0xFFFFu : 0xFFFFFFFFu);
+      const int b0 = t0 + 4 * bq;  // radii of tokens outside [t_lo, t_end) are cleared
+      const auto keep = [&](int j) { return b0 + j >= t_lo && b0 + j < t_end; };
+      vr.x &= (keep(0) ? 0xFFFFu : 0u) | (keep(1) ? 0xFFFF0000u : 0u);
+      vr.y &= (keep(2) ? 0xFFFFu : 0u) | (keep(3) ? 0xFFFF0000u : 0u);
     }
     half4_t pp[NSET];
 #pragma unroll
     for (int s = 0; s < NSET; ++s) {
       float4_t x = L[s];
-      if (!full && tk >= t_end) x = float4_t{kNegInf, kNegInf, kNegInf, kNegInf};
+      if (!full && (tk >= t_end || tk < t_lo)) x = float4_t{kNegInf, kNegInf, kNegInf, kNegInf};
       quad_transpose(x, lane);
       float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
       mx = xmax16(mx);
@@ -1005,7 +1032,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
 
   finish_unit<NSET>(smem, reinterpret_cast<int*>(smem + kGmeta), d, G, lz, kvh, split, tid, lane, wave, m_run, l_run,
                     O, counters, part, n_splits, 0.08838834764831845f /* 1/sqrt(d_h) */,
-                    reinterpret_cast<const float*>(blob + kOffRotV), out);
+                    reinterpret_cast<const float*>(blob + kOffRotV), out, win.part);
 }
 
 // ---------------------------------------------------------------- fp16 comparator
@@ -1210,7 +1237,7 @@ __global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __res
   }
   __syncthreads();
   finish_unit<NSET>(smem, reinterpret_cast<int*>(smem + kF16Flag), d, G, lz, kvh, split, tid, lane, wave, m_run, l_run,
-                    O, counters, part, n_splits, 1.f, nullptr, out);
+                    O, counters, part, n_splits, 1.f, nullptr, out, nullptr);
 }
 
 inline hipError_t launch_f16_mfma_impl(const Dims& d, const void* q, const int32_t* ctx_len, const void* k16,
@@ -1233,7 +1260,7 @@ hipError_t launch_split_bv_impl(const Dims& d, const void* layout, const void* q
   const uint8_t* blob = static_cast<const uint8_t*>(layout);
   const auto go = [&](auto kern) {
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, d, blob, q, ctx_len, c, out, ws.counters, ws.part,
-                       ws.n_splits, ws.split_len);
+                       ws.n_splits, ws.split_len, WinArgs{ws.wpart, ws.n_sink, ws.n_recent});
   };
   if (d.group <= 4) {
     if (d.k_words <= 8) go(k_split_mfma<1, 8, BV>);

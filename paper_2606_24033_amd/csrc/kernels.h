@@ -29,7 +29,35 @@ struct DecodeWs {
   float* part;        // [n_lc][batch][Hq][n_splits][130] (m, l, acc[128])
   int n_splits;       // splits actually launched
   int split_len;      // tokens per split, multiple of 64
+  // Protected fp16 window (null part: none).  The packed pass then covers
+  // rows [n_s, T - n_r) of a context of T rows, n_s = min(n_sink, T),
+  // n_r = min(n_recent, T - n_s), and the merge adds the window's partial
+  // [n_lc][batch][Hq][130] (m, l, acc[128] in the rotated V domain).
+  const float* wpart = nullptr;
+  int n_sink = 0, n_recent = 0;
 };
+
+// Window sizes: the sink must end inside the first 64-row tile (the packed
+// pass masks rows below it there only).
+constexpr int kMaxSink = 63;
+constexpr int kMaxRecent = 1024;
+
+// Kernel-side view of the window arguments.
+struct WinArgs {
+  const float* part;
+  int n_sink, n_recent;
+};
+
+// Protected window (a second fp16 store beside the packed cache): fp16
+// [n_layers][batch][n_kv][2][n_sink + n_recent][128], keys then values;
+// position t < n_sink sits in slot t, a later one in slot
+// n_sink + (t - n_sink) mod n_recent.
+hipError_t launch_window_append(const Dims& d, const void* k, const void* v, int n_new, const int32_t* write_pos,
+                                int n_sink, int n_recent, _Float16* window, hipStream_t s);
+// The window's attention partial of every (layer in call, sequence, query
+// head), written to wpart for the packed decode's merge.
+hipError_t launch_window_attn(const Dims& d, const void* layout, const void* q, const int32_t* ctx_len,
+                              const _Float16* window, int n_sink, int n_recent, float* wpart, hipStream_t s);
 
 // Packed decode (decode_impl.h), one entry per value code width
 // (decode_bv1.hip .. decode_bv8.hip): query rotation, split pass and the

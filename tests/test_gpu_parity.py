@@ -539,3 +539,62 @@ def test_llama_128k_step_sampled():
         log("llama 128k layer", layer, "head", head, "rel err", err, "ties", vars(stats))
         assert err <= P.tol_attention()
     assert stats.code_ties <= 1e-4 * stats.codes
+
+
+def test_protected_window_decode():
+    """Protected-buffer regime (sink 4 + recent 128 fp16 rows beside the packed
+    cache, and the 63 + 1 and 0 + 0 edges): a 100-row prefill that the window
+    covers (no packed rows), a 300-row chunk that overruns the recent ring, then
+    single-row decode appends; all-layer and single-layer calls, one and three
+    splits; against the oracle's protected attention within 2e-3, and the empty
+    window bit-identical to the plain packed decode."""
+    bg = bgm()
+    st = P.make_setup(11, 2, 2, 2, 4, 1024, 128, 2, 5e5, "bf16")
+    L, B, H, G = st.cfg.n_layers, st.cfg.batch, st.cfg.n_kv_heads, st.cfg.group
+    layout, cache = build(st)
+    windows = {(ns, nr): torch.zeros(bg.window_bytes(st.cfg, ns, nr) // 2, dtype=torch.float16, device="cuda")
+               for ns, nr in [(4, 128), (63, 1), (0, 0)]}
+    T_final = 403
+    kv = {(l, b, h): P.keys_values(st, l, h, 1000 * b, T_final) for l in range(L) for b in range(B) for h in range(H)}
+    rows = {key: P.oracle_rows(st, key[0], key[2], *kv[key]) for key in kv}
+    T = 0
+    worst = 0.0
+    for n in (100, 300, 1, 1, 1):
+        K = np.zeros((L, B, n, H, 128), np.float32)
+        V = np.zeros((L, B, n, H, 128), np.float32)
+        for (l, b, h), (k, v) in kv.items():
+            K[l, b, :, h], V[l, b, :, h] = k[T:T + n], v[T:T + n]
+        wp = torch.tensor([T] * B, dtype=torch.int32, device="cuda")
+        Kd, Vd = to_dev(K, st.dtype), to_dev(V, st.dtype)
+        bg.blockgtq_quantize_append(st.cfg, layout, -1, Kd, Vd, wp, cache)
+        for (ns, nr), win in windows.items():
+            bg.blockgtq_window_append(st.cfg, -1, Kd, Vd, wp, ns, nr, win)
+        T += n
+        q = np.stack([np.stack([np.concatenate([synth.cast(synth.queries(11, 16 * l + b, h, T - 1, G, 5e5, step=T),
+                                                           "bf16") for h in range(H)]) for b in range(B)])
+                      for l in range(L)])
+        qd = to_dev(q, "bf16")
+        ctx = torch.tensor([T] * B, dtype=torch.int32, device="cuda")
+        for (ns, nr), win in windows.items():
+            for n_splits in (0, 3):
+                log("protected window", ns, nr, "T", T, "splits", n_splits)
+                out = bg.blockgtq_decode_attn_protected(st.cfg, layout, -1, qd, ctx, T, cache, win, ns, nr,
+                                                        n_splits=n_splits).cpu().numpy().astype(np.float64)
+                if (ns, nr) == (0, 0):
+                    plain = bg.blockgtq_decode_attn(st.cfg, layout, -1, qd, ctx, T, cache, n_splits=n_splits)
+                    np.testing.assert_array_equal(out, plain.cpu().numpy())
+                for (l, b, h), (k, v) in kv.items():
+                    r = rows[l, b, h]
+                    bits = st.bits_oracle[l, h]
+                    kh = o.dequantize_keys(r.kcodes[:T], r.knorms[:T], bits, st.rot_k)
+                    vh = o.dequantize_values(r.vcodes[:T], r.vnorms[:T], st.rot_v, st.cfg.v_bits)
+                    ref = o.protected_attention(q[l, b, h * G:(h + 1) * G], kh, vh, o.fp16_round(k[:T]),
+                                                o.fp16_round(v[:T]), ns, nr)
+                    worst = max(worst, P.rel_err(out[l, b, h * G:(h + 1) * G], ref))
+        # a single-layer call reads the same window and cache
+        out1 = bg.blockgtq_decode_attn_protected(st.cfg, layout, 1, qd[1].contiguous(), ctx, T, cache,
+                                                 windows[4, 128], 4, 128).cpu().numpy().astype(np.float64)
+        allc = bg.blockgtq_decode_attn_protected(st.cfg, layout, -1, qd, ctx, T, cache, windows[4, 128], 4, 128)
+        np.testing.assert_allclose(out1, allc[1].cpu().numpy(), rtol=0, atol=1e-6)
+    log("protected window, max rel err", worst)
+    assert worst <= 2e-3

@@ -118,3 +118,42 @@ def test_prefill_sizes_and_argument_errors():
     assert call(ws=16) == -4
     assert call(q=ctypes.c_void_p(258)) == -1   # 4-byte alignment
     assert b"aligned" in L.blockgtq_last_error()
+
+
+def test_window_sizes_and_argument_errors():
+    """Host-side checks of the protected-window entry points (rejected before
+    any launch: the pointers are never dereferenced)."""
+    cfg = bg.Config(n_layers=2, batch=3, n_kv_heads=2, group=4, capacity=1024, k_budget=128, v_bits=2)
+    assert bg.window_bytes(cfg, 4, 128) == 2 * 3 * 2 * 2 * 132 * 128 * 2
+    assert bg.window_bytes(cfg, 0, 0) == 0
+    for ns, nr in [(64, 128), (-1, 0), (4, 1025), (0, -2)]:
+        with pytest.raises(bg.BlockGTQError) as e:
+            bg.window_bytes(cfg, ns, nr)
+        assert e.value.code == -1
+    base = bg.workspace_bytes(cfg, 2, 0, 1000)
+    assert bg.protected_workspace_bytes(cfg, 2, 0, 1000) == base + ((2 * 3 * 8 * 130 * 4 + 255) // 256) * 256
+    L = bg.lib()
+    c = cfg.c()
+    fake = ctypes.c_void_p(256)
+    cache = bg._Cache(256, 256, 256, 256)
+
+    def dec(layer=-1, ns=4, nr=128, ws=10 ** 9, max_ctx=1000, win=fake):
+        return L.blockgtq_decode_attn_protected(ctypes.byref(c), fake, layer, fake, fake, max_ctx,
+                                                ctypes.byref(cache), win, ns, nr, fake, fake, ws, 0, None)
+    assert dec(ns=64) == -1
+    assert dec(nr=2000) == -1
+    assert dec(layer=2) == -1
+    assert dec(max_ctx=1025) == -3
+    assert dec(win=None) == -1
+    assert dec(win=None, ns=0, nr=0, ws=16) == -4   # an empty window needs no buffer
+    assert dec(ws=base) == -4              # the window partials need room past the split partials
+
+    def app(layer=0, n_new=5, ns=4, nr=128, win=fake):
+        return L.blockgtq_window_append(ctypes.byref(c), layer, fake, fake, n_new, fake, ns, nr, win, None)
+    assert app(layer=5) == -1
+    assert app(n_new=-1) == -1
+    assert app(n_new=2000) == -3
+    assert app(ns=70) == -1
+    assert app(n_new=0) == 0               # nothing to write
+    assert app(ns=0, nr=0) == 0            # no window
+    assert app(win=None) == -1

@@ -389,3 +389,51 @@ def test_blockgtq_beats_uniform_logit_mae_direction():
             kh = o.dequantize_keys(c, n, bits, rot_k)
             err[name] = np.mean(np.abs(np.sum(q * (k - kh), axis=1)))
         assert err["gtq"] < err["uni"]
+
+
+def test_protected_window_pins():
+    """Protected-buffer regime (Sec. 6, reasoning evaluation; buffer
+    configurations of its appendix): no window is the packed-only attention;
+    a window that covers the context is plain fp16 attention (torch's CPU
+    scaled_dot_product_attention in float64); and a value perturbation that is
+    one-hot per position shows exactly which positions are read from fp16, each
+    weighted by its softmax probability (scipy)."""
+    import torch
+    from scipy.special import softmax
+    rng = np.random.default_rng(41)
+    d, G = 128, 4
+    for T, ns, nr in [(100, 4, 20), (128, 0, 7), (57, 5, 0), (3, 4, 128), (132, 4, 128), (200, 63, 1)]:
+        q = rng.standard_normal((G, d)) * 2.0
+        kh = rng.standard_normal((T, d))
+        vh = rng.standard_normal((T, d))
+        k16 = o.fp16_round(kh + 0.1 * rng.standard_normal((T, d)))
+        v16 = o.fp16_round(vh + 0.1 * rng.standard_normal((T, d)))
+        # no window: the packed rows only
+        np.testing.assert_array_equal(o.protected_attention(q, kh, vh, k16, v16, 0, 0), o.attention(q, kh, vh))
+        # a window that covers the context: plain attention over the fp16 rows
+        if T <= ns + nr:
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                torch.from_numpy(q)[None], torch.from_numpy(k16)[None], torch.from_numpy(v16)[None])[0].numpy()
+            np.testing.assert_allclose(o.protected_attention(q, kh, vh, k16, v16, ns, nr), ref, rtol=1e-12, atol=1e-13)
+        # which rows come from fp16: equal keys, values perturbed by delta e_(t mod d)
+        if T <= d:
+            delta = 1e-3
+            v16b = vh + delta * np.eye(T, d)
+            diff = o.protected_attention(q, kh, vh, kh, v16b, ns, nr) - o.attention(q, kh, vh)
+            p = softmax(q @ kh.T / math.sqrt(d), axis=1)
+            n_s = min(ns, T)
+            n_r = min(nr, T - n_s)
+            window = set(range(n_s)) | set(range(T - n_r, T))
+            want = np.zeros((G, d))
+            for t in window:
+                want[:, t] = delta * p[:, t]
+            np.testing.assert_allclose(diff, want, rtol=1e-9, atol=1e-15)
+    # a planted off-by-one (the recent window one row short) fails the last check
+    T, ns, nr = 60, 4, 10
+    q = rng.standard_normal((G, d))
+    kh = rng.standard_normal((T, d))
+    vh = rng.standard_normal((T, d))
+    v16b = vh + 1e-3 * np.eye(T, d)
+    good = o.protected_attention(q, kh, vh, kh, v16b, ns, nr)
+    short = o.protected_attention(q, kh, vh, kh, v16b, ns, nr - 1)
+    assert np.abs(good - short)[:, T - nr].min() > 1e-8
