@@ -31,6 +31,7 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2606_24033_amd", "csrc", "decode_impl.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_split_mfma_llama8b_128k_k2v2_traffic.json")
 SEED = 3
 N_LAYERS, N_KV, GROUP, BASE = 32, 8, 4, 5e5
+N_SINK, N_RECENT = 4, 128      # protected-buffer regime of the reasoning evaluation
 K_BUDGET, V_BITS = 128, 2
 N_CAL = 2048
 
@@ -53,6 +54,8 @@ def parse():
     ap.add_argument("--prefill-len", type=int, default=32768)
     ap.add_argument("--no-uniform", action="store_true",
                     help="skip the uniform TQ-MSE K layout (one K group per head) comparison")
+    ap.add_argument("--no-protected", action="store_true",
+                    help="skip the protected fp16 window (4 sink + 128 recent rows) measurement")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one plain device copy of this size first (HBM counter calibration)")
@@ -179,6 +182,37 @@ def uniform_comparison(bg, synth, torch, cfg, rot_k, rot_v, sig, T, n_extra, q_a
     return res
 
 
+def protected_measurement(bg, torch, cfg, layout, cache, window, knew_all, vnew_all, wps, q_all, ctxs, max_ctx, args,
+                          dec_med):
+    """The same decode in the protected-buffer regime: the first N_SINK and the
+    last N_RECENT rows of every (layer, KV head) served from an fp16 window
+    (blockgtq_decode_attn_protected: the window kernel, then the packed decode
+    over the rows in between).  Decode calls only, at the timed steps'
+    contexts; the window holds the step rows too (appended after the timed
+    loop, so the ring holds the last context's recent rows)."""
+    for s in range(wps.numel()):
+        bg.blockgtq_window_append(cfg, -1, knew_all[s], vnew_all[s], wps[s:s + 1], N_SINK, N_RECENT, window)
+    wout = torch.empty_like(q_all[0], dtype=torch.float32)
+    wws = torch.zeros(bg.protected_workspace_bytes(cfg, N_LAYERS, args.n_splits, max_ctx), dtype=torch.uint8,
+                      device="cuda")
+    for i in range(args.warmup):
+        s = args.warmup + i % args.steps
+        bg.blockgtq_decode_attn_protected(cfg, layout, -1, q_all[s], ctxs[s:s + 1], max_ctx, cache, window, N_SINK,
+                                          N_RECENT, out=wout, workspace=wws, n_splits=args.n_splits)
+    pe = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for i in range(args.steps):
+        s = args.warmup + i
+        pe[i][0].record()
+        bg.blockgtq_decode_attn_protected(cfg, layout, -1, q_all[s], ctxs[s:s + 1], max_ctx, cache, window, N_SINK,
+                                          N_RECENT, out=wout, workspace=wws, n_splits=args.n_splits)
+        pe[i][1].record()
+    torch.cuda.synchronize()
+    p_us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in pe]))
+    return {"n_sink": N_SINK, "n_recent": N_RECENT, "decode_us_median": round(p_us, 2),
+            "time_over_no_buffer": round(p_us / dec_med, 3),
+            "kernels": "k_window_attn + k_split_mfma (packed rows between the windows)"}
+
+
 def prefill_measurement(bg, synth, torch, bits, sig, rot_k, rot_v, T):
     """Causal prefill attention over the packed cache for one layer of the same
     model shape: a T-token prompt quantized into a one-layer cache (layer 0's
@@ -261,10 +295,16 @@ def main():
         k16 = torch.zeros((N_LAYERS, 1, N_KV, cap, 128), dtype=torch.float16, device="cuda")
         v16 = torch.zeros_like(k16)
     wp0 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    want_win = not args.no_protected
+    if want_win:
+        window = torch.zeros(bg.window_bytes(cfg, N_SINK, N_RECENT) // 2, dtype=torch.float16, device="cuda")
     for layer in range(N_LAYERS):
         k, v = synth.torch_layer_kv(SEED, layer, T + n_extra, sig[layer], BASE)
         bg.blockgtq_quantize_append(cfg, layout, layer, k[None, :T].contiguous(), v[None, :T].contiguous(), wp0,
                                     cache)
+        if want_win:
+            bg.blockgtq_window_append(cfg, layer, k[None, :T].contiguous(), v[None, :T].contiguous(), wp0, N_SINK,
+                                      N_RECENT, window)
         if want_fp16:
             k16[layer, 0, :, :T + n_extra] = k.transpose(0, 1).half()
             v16[layer, 0, :, :T + n_extra] = v.transpose(0, 1).half()
@@ -383,6 +423,11 @@ def main():
         result["fp16_decode_gbs"] = round(fbytes / (f_us * 1e-6) / 1e9, 2)
         result["speedup_vs_fp16_decode"] = round(f_us / dec_med, 3)
         del k16, v16
+
+    if want_win:
+        result["protected_window"] = protected_measurement(bg, torch, cfg, layout, cache, window, knew_all, vnew_all,
+                                                           wps, q_all, ctxs, max_ctx, args, dec_med)
+        del window
 
     if not args.no_prefill:
         result["prefill_attn"] = prefill_measurement(bg, synth, torch, bits, sig, rot_k, rot_v, args.prefill_len)

@@ -15,6 +15,8 @@ Conventions (one KV head, head dim d_h, L = d_h / 2 RoPE blocks):
   midpoints of adjacent fp16 centroids                             [READING Q1]
 * a value exactly on a threshold takes the upper code              [READING T2]
 * zero vector: stored norm 0, every code 2^(b-1)                   [READING Z1]
+* protected window: the first n_sink and last n_recent rows of a context
+  use their fp16 K/V, the rest the dequantized ones                 [READING W1]
 """
 from __future__ import annotations
 
@@ -450,7 +452,8 @@ def protected_attention(q: np.ndarray, k_hat: np.ndarray, v_hat: np.ndarray, k16
     n_r = min(n_recent, T - n_s) keep their fp16 keys/values (k16, v16,
     [T, d], already fp16-rounded), the rows in between are the dequantized
     ones (k_hat, v_hat).  Definition mode: the keys and values of every row
-    are picked, then one softmax over all T rows.  q [Hg, d] -> [Hg, d]."""
+    are picked, then one softmax over all T rows.  q [Hg, d] -> [Hg, d].
+    [READING W1]"""
     T = k_hat.shape[0]
     ns = min(n_sink, T)
     nr = min(n_recent, T - ns)

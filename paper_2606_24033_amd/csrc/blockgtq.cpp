@@ -635,8 +635,8 @@ int blockgtq_decode_attn_protected(const bgtq_config* cfg, const void* d_layout,
   ws.n_recent = n_recent;
   const Dims d = dims_of(cfg, layer);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = launch_window_attn(d, d_layout, d_q, d_ctx_len, static_cast<const _Float16*>(d_window), n_sink,
-                                    n_recent, wpart, s);
+  hipError_t e = launch_window_attn(d, d_q, d_ctx_len, static_cast<const _Float16*>(d_window), n_sink, n_recent,
+                                    wpart, s);
   if (e != hipSuccess) return hip_fail(e, "window_attn launch");
   CachePtrs c{static_cast<uint32_t*>(cache->k_codes), static_cast<uint16_t*>(cache->k_norms),
               static_cast<uint32_t*>(cache->v_codes), static_cast<uint16_t*>(cache->v_norms)};

@@ -548,16 +548,20 @@ __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const
 // the V rotation (rotv) or none, o scaled by oscale.  The merge area of LDS
 // starts at smem; `last` is a flag word outside it.
 // Log-sum-exp merge of the protected window's partial (m, l, acc[128], written
-// by the window kernel before this launch) into a running (mx, l, a).
-__device__ __forceinline__ void merge_window(const float* __restrict__ w, int dd, float& mx, float& l, float& a) {
+// by the window kernel before this launch) into a running (mx, l, a).  The
+// window's accumulator is in the original V domain: it is added after the
+// output rotation, with the weight returned here (its share of the merged
+// sum still to be divided by the final l).
+__device__ __forceinline__ float merge_window(const float* __restrict__ w, float& mx, float& l, float& a) {
   const float mw = w[0];
-  if (mw == kNegInf) return;
+  if (mw == kNegInf) return 0.f;
   const float mc = fmaxf(mx, mw);
   const float r = mx == kNegInf ? 0.f : exp2_hw(mx - mc);
   const float e = exp2_hw(mw - mc);
   l = fmaf(w[1], e, l * r);
-  a = fmaf(w[2 + dd], e, a * r);
+  a *= r;
   mx = mc;
+  return e;
 }
 
 template <int NSET>
@@ -590,6 +594,7 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
   }
   __syncthreads();
   float* os = fo + kWaves * 8 * kHeadDim;  // [G][128] merged output, rotated V domain
+  float* ws_ = os + 8 * kHeadDim;          // [G][128] weight of the window's accumulator
   for (int i = tid; i < G * kHeadDim; i += kThreads) {
     const int qh = i >> 7, dd = i & 127;
     float mx = kNegInf;
@@ -605,8 +610,10 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
       }
     }
     if (n_splits == 1) {
-      if (wpart != nullptr) merge_window(wpart + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * 130, dd, mx, l, a);
+      float e = 0.f;
+      if (wpart != nullptr) e = merge_window(wpart + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * 130, mx, l, a);
       os[i] = l > 0.f ? a / l * oscale : 0.f;
+      if (wpart != nullptr) ws_[i] = l > 0.f ? e / l : 0.f;
     } else {
       // device-coherent stores (no L2 write-back needed before the counter)
       float* pb = part + ((static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits + split) * 130;
@@ -667,8 +674,10 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
         }
         mx = mc;
       }
-      if (wpart != nullptr) merge_window(wpart + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * 130, dd, mx, l, a);
+      float e = 0.f;
+      if (wpart != nullptr) e = merge_window(wpart + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * 130, mx, l, a);
       os[i] = l > 0.f ? a / l * oscale : 0.f;
+      if (wpart != nullptr) ws_[i] = l > 0.f ? e / l : 0.f;
     }
     if (tid == 0) __hip_atomic_store(counters + lz * d.n_kv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -681,6 +690,7 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
       r = 0.f;
       for (int jj = 0; jj < kHeadDim; ++jj) r = fmaf(rotv[jj * kHeadDim + dd], os[qh * kHeadDim + jj], r);
     }
+    if (wpart != nullptr) r = fmaf(ws_[i], wpart[(static_cast<size_t>(lz) * hqn + kvh * G + qh) * 130 + 2 + dd], r);
     out[(static_cast<size_t>(lz) * hqn + kvh * G + qh) * kHeadDim + dd] = r;
   }
 }
@@ -1043,7 +1053,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
 // flight.  Values: lane = dim gathers each 4-token step with 2-byte loads
 // (every load instruction reads one row's 128 contiguous bytes), half of a
 // tile issued with its keys and the other half after its QK products.
-constexpr int kF16Flag = (kWaves * 8 * 2 + kWaves * 8 * kHeadDim + 8 * kHeadDim) * 4;  // past the merge area
+constexpr int kF16Flag = (kWaves * 8 * 2 + kWaves * 8 * kHeadDim + 2 * 8 * kHeadDim) * 4;  // past the merge area
 constexpr int kF16Lds = kF16Flag + 16;
 
 template <int NSET, int S0, int... J>

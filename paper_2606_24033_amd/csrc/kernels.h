@@ -32,7 +32,7 @@ struct DecodeWs {
   // Protected fp16 window (null part: none).  The packed pass then covers
   // rows [n_s, T - n_r) of a context of T rows, n_s = min(n_sink, T),
   // n_r = min(n_recent, T - n_s), and the merge adds the window's partial
-  // [n_lc][batch][Hq][130] (m, l, acc[128] in the rotated V domain).
+  // [n_lc][batch][Hq][130] (m, l, acc[128] in the original V domain).
   const float* wpart = nullptr;
   int n_sink = 0, n_recent = 0;
 };
@@ -56,8 +56,8 @@ hipError_t launch_window_append(const Dims& d, const void* k, const void* v, int
                                 int n_sink, int n_recent, _Float16* window, hipStream_t s);
 // The window's attention partial of every (layer in call, sequence, query
 // head), written to wpart for the packed decode's merge.
-hipError_t launch_window_attn(const Dims& d, const void* layout, const void* q, const int32_t* ctx_len,
-                              const _Float16* window, int n_sink, int n_recent, float* wpart, hipStream_t s);
+hipError_t launch_window_attn(const Dims& d, const void* q, const int32_t* ctx_len, const _Float16* window,
+                              int n_sink, int n_recent, float* wpart, hipStream_t s);
 
 // Packed decode (decode_impl.h), one entry per value code width
 // (decode_bv1.hip .. decode_bv8.hip): query rotation, split pass and the

@@ -7,9 +7,9 @@
 // Two kernels:
 //  * k_window_append: copies appended K/V rows into the window (fp16);
 //  * k_window_attn: per (layer in call, sequence, KV head), the attention
-//    partial of the G query heads over the window rows, in the packed
-//    decode's units (base-2 logits, accumulator in the rotated V domain
-//    scaled by sqrt(d_h)), which the packed decode's merge folds in.
+//    partial of the G query heads over the window rows (base-2 logits as in
+//    the packed decode, accumulator in the original V domain), which the
+//    packed decode's merge folds in.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -59,15 +59,14 @@ __global__ __launch_bounds__(kHeadDim) void k_window_append(Dims d, const void* 
 // grid (n_kv, n_lc * batch), 256 threads.  Rows of the window at context T:
 // n_s = min(n_sink, T) sink rows and n_r = min(n_recent, T - n_s) recent rows
 // T - n_r .. T - 1 (the packed decode covers the rows in between).
-__global__ __launch_bounds__(kWinThreads) void k_window_attn(Dims d, const float* __restrict__ rotvt,
-                                                             const void* __restrict__ q,
+__global__ __launch_bounds__(kWinThreads) void k_window_attn(Dims d, const void* __restrict__ q,
                                                              const int32_t* __restrict__ ctx_len,
                                                              const _Float16* __restrict__ win, int n_sink,
                                                              int n_recent, float* __restrict__ wpart) {
   __shared__ float qs[8][kHeadDim];
   __shared__ float sc[8][kMaxWinRows];
-  __shared__ float acc[8][kHeadDim];
   __shared__ float ml[8][2];
+  __shared__ float red[kWinThreads / 64][8][kHeadDim];
   const int kvh = blockIdx.x, lz = blockIdx.y;
   const int seq = lz % d.batch;
   const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
@@ -128,37 +127,40 @@ __global__ __launch_bounds__(kWinThreads) void k_window_attn(Dims d, const float
   }
   __syncthreads();
 
-  // sum_j p_j v_j (lane = dim, coalesced value rows)
+  // sum_j p_j v_j in the original V domain (the packed decode adds it after
+  // its output rotation): lane = a pair of dims, wave w takes the rows
+  // j = w mod 4 (one coalesced 256-byte row read per wave and row), then the
+  // four waves' sums are added through LDS
+  float2 acc[8];
+#pragma unroll
+  for (int g = 0; g < 8; ++g) acc[g] = make_float2(0.f, 0.f);
+#pragma unroll 4
+  for (int j = wave; j < W; j += kWinThreads / 64) {
+    const int t = j < ns ? j : T - nr + (j - ns);
+    const uint32_t vv =
+        *reinterpret_cast<const uint32_t*>(vb + static_cast<size_t>(win_slot(t, n_sink, n_recent)) * kHeadDim + 2 * lane);
+    const float v0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(vv & 0xFFFFu)));
+    const float v1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(vv >> 16)));
+#pragma unroll
+    for (int g = 0; g < 8; ++g)
+      if (g < G) {
+        acc[g].x = fmaf(sc[g][j], v0, acc[g].x);
+        acc[g].y = fmaf(sc[g][j], v1, acc[g].y);
+      }
+  }
+#pragma unroll
+  for (int g = 0; g < 8; ++g)
+    if (g < G) {
+      red[wave][g][2 * lane] = acc[g].x;
+      red[wave][g][2 * lane + 1] = acc[g].y;
+    }
+  __syncthreads();
   for (int i = tid; i < G * kHeadDim; i += kWinThreads) {
     const int g = i >> 7, dd = i & 127;
-    float a = 0.f;
-    for (int j = 0; j < W; ++j) {
-      const int t = j < ns ? j : T - nr + (j - ns);
-      a = fmaf(sc[g][j], static_cast<float>(vb[static_cast<size_t>(win_slot(t, n_sink, n_recent)) * kHeadDim + dd]), a);
-    }
-    acc[g][dd] = a;
-  }
-  __syncthreads();
-
-  // into the packed decode's accumulator domain: sqrt(d_h) Pi_V a
-  // (rotvt[dd][jj] = Pi_V[jj][dd], coalesced over jj)
-  const int jj = tid & 127, g0 = tid >> 7;
-  float r[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int dd = 0; dd < kHeadDim; ++dd) {
-    const float pv = rotvt[dd * kHeadDim + jj];
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (g0 + 2 * u < G) r[u] = fmaf(pv, acc[g0 + 2 * u][dd], r[u]);
-  }
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int g = g0 + 2 * u;
-    if (g < G) {
-      wp[g * 130 + 2 + jj] = r[u] * 11.313708498984761f;  // sqrt(d_h)
-      if (jj == 0) {
-        wp[g * 130] = ml[g][0];
-        wp[g * 130 + 1] = ml[g][1];
-      }
+    wp[g * 130 + 2 + dd] = (red[0][g][dd] + red[1][g][dd]) + (red[2][g][dd] + red[3][g][dd]);
+    if (dd == 0) {
+      wp[g * 130] = ml[g][0];
+      wp[g * 130 + 1] = ml[g][1];
     }
   }
 }
@@ -173,12 +175,10 @@ hipError_t launch_window_append(const Dims& d, const void* k, const void* v, int
   return hipGetLastError();
 }
 
-hipError_t launch_window_attn(const Dims& d, const void* layout, const void* q, const int32_t* ctx_len,
-                              const _Float16* window, int n_sink, int n_recent, float* wpart, hipStream_t s) {
-  const float* rotvt = reinterpret_cast<const float*>(static_cast<const uint8_t*>(layout) + kOffRotVT);
+hipError_t launch_window_attn(const Dims& d, const void* q, const int32_t* ctx_len, const _Float16* window,
+                              int n_sink, int n_recent, float* wpart, hipStream_t s) {
   dim3 grid(d.n_kv, d.n_lc * d.batch);
-  hipLaunchKernelGGL(k_window_attn, grid, dim3(kWinThreads), 0, s, d, rotvt, q, ctx_len, window, n_sink, n_recent,
-                     wpart);
+  hipLaunchKernelGGL(k_window_attn, grid, dim3(kWinThreads), 0, s, d, q, ctx_len, window, n_sink, n_recent, wpart);
   return hipGetLastError();
 }
 
