@@ -271,6 +271,36 @@ int blockgtq_decode_attn_protected(const bgtq_config* cfg, const void* d_layout,
                                    const void* d_window, int32_t n_sink, int32_t n_recent, float* d_out,
                                    void* d_workspace, size_t ws_bytes, int32_t n_splits, void* stream);
 
+/* ---- (f2) decode step from pre-RoPE inputs --------------------------------
+ * One decode step of every layer with RoPE applied on the device (Sec. 2.1:
+ * block i = dims (i, i + 64) of a vector at position t is rotated by the angle
+ * t * theta_i, theta_i = rope_base^(-2i/d_h); Sec. 2.3, the absolute rotation
+ * R_t).  The angle is formed and reduced in fp64.  Three launches on `stream`,
+ * no allocation, no memset, so the step can be captured in a HIP graph and
+ * replayed with new inputs written into the same buffers:
+ *   1. RoPE of the query and key rows at position d_pos[b], into fp32
+ *      workspace rows (the value row is copied to fp32 beside them), and
+ *      ctx[b] = d_pos[b] + 1;
+ *   2. blockgtq_quantize_append of the rotated key and the value at row
+ *      d_pos[b] of every layer;
+ *   3. blockgtq_decode_attn of every layer over rows [0, d_pos[b] + 1).
+ * d_q_pre: pre-RoPE queries [n_layers][batch][n_kv_heads*group][128],
+ * d_k_pre, d_v: [n_layers][batch][1][n_kv_heads][128], all in in_dtype.
+ * d_pos: device int32 [batch], the new row's position; the caller keeps
+ *      d_pos[b] < capacity (rows past it are not written, the context is
+ *      clamped) and max_ctx >= every d_pos[b] + 1 (it sizes the splits;
+ *      rows past n_splits x split length are not read).
+ * rope_base: theta base, finite and > 1 (EINVAL otherwise).
+ * d_out: float [n_layers][batch][n_kv_heads*group][128].
+ * d_workspace: blockgtq_rope_step_workspace_bytes; its first part is a
+ *      blockgtq_decode_attn workspace (zero-filled once before first use). */
+int blockgtq_rope_step_workspace_bytes(const bgtq_config* cfg, int32_t max_ctx, int32_t n_splits,
+                                       size_t* bytes_out);
+int blockgtq_rope_decode_step(const bgtq_config* cfg, const void* d_layout, double rope_base, const void* d_q_pre,
+                              const void* d_k_pre, const void* d_v, const int32_t* d_pos, int32_t max_ctx,
+                              const bgtq_cache* cache, float* d_out, void* d_workspace, size_t ws_bytes,
+                              int32_t n_splits, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

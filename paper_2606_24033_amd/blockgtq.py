@@ -26,7 +26,7 @@ EXPORTED = [
     "blockgtq_layout_init", "blockgtq_quantize_append", "blockgtq_decode_attn",
     "blockgtq_decode_attn_fp16", "blockgtq_prefill_workspace_bytes", "blockgtq_prefill_attn",
     "blockgtq_window_bytes", "blockgtq_window_append", "blockgtq_protected_workspace_bytes",
-    "blockgtq_decode_attn_protected",
+    "blockgtq_decode_attn_protected", "blockgtq_rope_step_workspace_bytes", "blockgtq_rope_decode_step",
 ]
 
 
@@ -77,6 +77,8 @@ def lib():
             "blockgtq_window_append": [P, I32, P, P, I32, P, I32, I32, P, P],
             "blockgtq_protected_workspace_bytes": [P, I32, I32, I32, PSZ],
             "blockgtq_decode_attn_protected": [P, P, I32, P, P, I32, P, P, I32, I32, P, P, SZ, I32, P],
+            "blockgtq_rope_step_workspace_bytes": [P, I32, I32, PSZ],
+            "blockgtq_rope_decode_step": [P, P, ctypes.c_double, P, P, P, P, I32, P, P, P, SZ, I32, P],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -345,4 +347,32 @@ def blockgtq_decode_attn_protected(cfg: Config, layout: Layout, layer: int, q, c
                                                 _ptr(ctx_len), max_ctx, ctypes.byref(cache.c()), _ptr(window),
                                                 n_sink, n_recent, _ptr(out), _ptr(workspace), workspace.numel(),
                                                 n_splits, _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------- decode step from pre-RoPE inputs
+
+def rope_step_workspace_bytes(cfg: Config, max_ctx: int, n_splits: int = 0) -> int:
+    v = ctypes.c_size_t()
+    _check(lib().blockgtq_rope_step_workspace_bytes(ctypes.byref(cfg.c()), max_ctx, n_splits, ctypes.byref(v)))
+    return v.value
+
+
+def blockgtq_rope_decode_step(cfg: Config, layout: Layout, rope_base: float, q_pre, k_pre, v, pos, max_ctx: int,
+                              cache: Cache, out=None, workspace=None, n_splits: int = 0, stream=None):
+    """One all-layer decode step from pre-RoPE q [L, B, Hq, 128] and k, v
+    [L, B, 1, H_kv, 128] (in_dtype) at device positions pos (int32 [B])."""
+    import torch
+    for t in (q_pre, k_pre, v):
+        _check_dev(t, _in_dtype(cfg))
+    _check_dev(pos, torch.int32)
+    if out is None:
+        out = torch.empty(q_pre.shape, dtype=torch.float32, device=q_pre.device)
+    if workspace is None:
+        workspace = torch.zeros(rope_step_workspace_bytes(cfg, max_ctx, n_splits), dtype=torch.uint8,
+                                device=q_pre.device)
+    _check(lib().blockgtq_rope_decode_step(ctypes.byref(cfg.c()), _ptr(layout.blob), float(rope_base), _ptr(q_pre),
+                                           _ptr(k_pre), _ptr(v), _ptr(pos), max_ctx, ctypes.byref(cache.c()),
+                                           _ptr(out), _ptr(workspace), workspace.numel(), n_splits,
+                                           _stream(stream)))
     return out

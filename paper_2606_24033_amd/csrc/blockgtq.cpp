@@ -645,6 +645,72 @@ int blockgtq_decode_attn_protected(const bgtq_config* cfg, const void* d_layout,
   return ok();
 }
 
+// Workspace of the pre-RoPE step: the decode workspace, then ctx int32
+// [batch], RoPE'd q fp32 [n_layers][batch][Hq][128], k and v fp32
+// [n_layers][batch][n_kv][128].
+struct StepWs {
+  size_t decode, ctx, q, k, v, total;
+};
+static StepWs step_ws(const bgtq_config* cfg, int32_t max_ctx, int32_t n_splits) {
+  StepWs w;
+  w.decode = ws_bytes_of(cfg, cfg->n_layers, plan_splits(cfg, cfg->n_layers, max_ctx, n_splits));
+  const size_t lb = static_cast<size_t>(cfg->n_layers) * cfg->batch;
+  w.ctx = w.decode;
+  w.q = w.ctx + al256(4 * static_cast<size_t>(cfg->batch));
+  w.k = w.q + al256(lb * cfg->n_kv_heads * cfg->group * kHeadDim * 4);
+  w.v = w.k + al256(lb * cfg->n_kv_heads * kHeadDim * 4);
+  w.total = w.v + al256(lb * cfg->n_kv_heads * kHeadDim * 4);
+  return w;
+}
+
+int blockgtq_rope_step_workspace_bytes(const bgtq_config* cfg, int32_t max_ctx, int32_t n_splits,
+                                       size_t* bytes_out) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!bytes_out) return fail(BGTQ_EINVAL, "NULL pointer");
+  if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);
+  if (max_ctx < 0 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [0, capacity]", max_ctx);
+  *bytes_out = step_ws(cfg, max_ctx, n_splits).total;
+  return ok();
+}
+
+int blockgtq_rope_decode_step(const bgtq_config* cfg, const void* d_layout, double rope_base, const void* d_q_pre,
+                              const void* d_k_pre, const void* d_v, const int32_t* d_pos, int32_t max_ctx,
+                              const bgtq_cache* cache, float* d_out, void* d_workspace, size_t ws_bytes,
+                              int32_t n_splits, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (!d_layout || !d_q_pre || !d_k_pre || !d_v || !d_pos || !d_out || !d_workspace || !cache || !cache->k_codes ||
+      !cache->k_norms || !cache->v_codes || !cache->v_norms)
+    return fail(BGTQ_EINVAL, "NULL pointer");
+  if (!(rope_base > 1.0) || !std::isfinite(rope_base)) return fail(BGTQ_EINVAL, "rope_base must be finite and > 1");
+  if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);
+  if (max_ctx < 1 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [1, capacity]", max_ctx);
+  const StepWs w = step_ws(cfg, max_ctx, n_splits);
+  if (ws_bytes < w.total) return fail(BGTQ_EWORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, w.total);
+  uint8_t* base = static_cast<uint8_t*>(d_workspace);
+  int32_t* ctx = reinterpret_cast<int32_t*>(base + w.ctx);
+  float* qo = reinterpret_cast<float*>(base + w.q);
+  float* ko = reinterpret_cast<float*>(base + w.k);
+  float* vo = reinterpret_cast<float*>(base + w.v);
+  Dims d = dims_of(cfg, -1);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_rope_step(d, rope_base, d_q_pre, d_k_pre, d_v, d_pos, qo, ko, vo, ctx, s);
+  if (e != hipSuccess) return hip_fail(e, "rope_step launch");
+  d.in_dtype = BGTQ_FP32;  // the append and the decode read the fp32 RoPE'd rows
+  CachePtrs c{static_cast<uint32_t*>(cache->k_codes), static_cast<uint16_t*>(cache->k_norms),
+              static_cast<uint32_t*>(cache->v_codes), static_cast<uint16_t*>(cache->v_norms)};
+  e = launch_quantize_append(d, d_layout, ko, vo, 1, d_pos, c, s);
+  if (e != hipSuccess) return hip_fail(e, "rope_step append launch");
+  const SplitPlan p = plan_splits(cfg, cfg->n_layers, max_ctx, n_splits);
+  DecodeWs ws;
+  ws.counters = static_cast<int32_t*>(d_workspace);
+  ws.part = reinterpret_cast<float*>(base + ws_counter_bytes(cfg, cfg->n_layers));
+  ws.n_splits = p.n_splits;
+  ws.split_len = p.split_len;
+  e = launch_decode_packed(d, d_layout, qo, ctx, c, d_out, ws, s);
+  if (e != hipSuccess) return hip_fail(e, "rope_step decode launch");
+  return ok();
+}
+
 int blockgtq_prefill_workspace_bytes(const bgtq_config* cfg, int32_t n_q, size_t* bytes_out) {
   if (int e = check_cfg(cfg)) return e;
   if (!bytes_out) return fail(BGTQ_EINVAL, "NULL pointer");

@@ -42,6 +42,11 @@ struct DecodeWs {
 constexpr int kMaxSink = 63;
 constexpr int kMaxRecent = 1024;
 
+// Pre-RoPE decode-step inputs -> RoPE'd fp32 q, k and fp32 v (same layouts
+// as the decode / append inputs of one row), and ctx[b] = pos[b] + 1.
+hipError_t launch_rope_step(const Dims& d, double base, const void* q, const void* k, const void* v,
+                            const int32_t* pos, float* qo, float* ko, float* vo, int32_t* ctx, hipStream_t s);
+
 // Kernel-side view of the window arguments.
 struct WinArgs {
   const float* part;

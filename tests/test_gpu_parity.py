@@ -598,3 +598,113 @@ def test_protected_window_decode():
         np.testing.assert_allclose(out1, allc[1].cpu().numpy(), rtol=0, atol=1e-6)
     log("protected window, max rel err", worst)
     assert worst <= 2e-3
+
+
+def _pre_rope(x, pos, base):
+    """Undo the synthetic generator's RoPE: R_(-pos) x, fp64 (test-local)."""
+    return o.rope_absolute(np.asarray(x, np.float64), -float(pos), base)
+
+
+def test_rope_decode_step_against_oracle():
+    """Decode steps from pre-RoPE inputs (on-device RoPE at position 300..302
+    of a 300-row prefill, fp32 inputs, batch 2, 2 layers, G = 4): the appended
+    codes against the oracle's quantization of its own RoPE of the same
+    pre-RoPE rows (ties counted), the outputs against the oracle within 2e-3."""
+    bg = bgm()
+    base = 5e5
+    st = P.make_setup(12, 2, 2, 2, 4, 512, 128, 2, base, "fp32")
+    L, B, H, G = st.cfg.n_layers, st.cfg.batch, st.cfg.n_kv_heads, st.cfg.group
+    layout, cache = build(st)
+    T0, n_steps = 300, 3
+    kv = {(l, b, h): P.keys_values(st, l, h, 1000 * b, T0 + n_steps) for l in range(L) for b in range(B)
+          for h in range(H)}
+    for l in range(L):
+        append(st, layout, cache, l, [[(kv[l, b, h][0][:T0], kv[l, b, h][1][:T0]) for h in range(H)]
+                                      for b in range(B)], [0] * B)
+    # the oracle's rows: prefill rows as given, step rows re-derived from the pre-RoPE input
+    krows = {key: np.array(kv[key][0][:T0 + n_steps], np.float64) for key in kv}
+    stats = P.Stats()
+    worst = 0.0
+    ws = torch.zeros(bg.rope_step_workspace_bytes(st.cfg, T0 + n_steps), dtype=torch.uint8, device="cuda")
+    for s in range(n_steps):
+        pos = T0 + s
+        kpre = np.zeros((L, B, 1, H, 128), np.float32)
+        vv = np.zeros((L, B, 1, H, 128), np.float32)
+        qpre = np.zeros((L, B, H * G, 128), np.float32)
+        qpost = np.zeros((L, B, H * G, 128), np.float64)
+        for (l, b, h), (k, v) in kv.items():
+            kpre[l, b, 0, h] = _pre_rope(k[pos], pos, base)
+            vv[l, b, 0, h] = v[pos]
+            krows[l, b, h][pos] = np.float32(o.rope_absolute(kpre[l, b, 0, h].astype(np.float64), pos, base))
+            qp = synth.queries(12, 16 * l + b, h, pos, G, base, step=pos)
+            qpre[l, b, h * G:(h + 1) * G] = _pre_rope(qp, pos, base)
+            qpost[l, b, h * G:(h + 1) * G] = o.rope_absolute(qpre[l, b, h * G:(h + 1) * G].astype(np.float64), pos,
+                                                             base)
+        posd = torch.tensor([pos] * B, dtype=torch.int32, device="cuda")
+        log("rope step", s, "position", pos)
+        out = bg.blockgtq_rope_decode_step(st.cfg, layout, base, to_dev(qpre, "fp32"), to_dev(kpre, "fp32"),
+                                           to_dev(vv, "fp32"), posd, T0 + n_steps, cache, workspace=ws)
+        out = out.cpu().numpy().astype(np.float64)
+        for (l, b, h), (k, v) in kv.items():
+            rows = P.oracle_rows(st, l, h, krows[l, b, h][:pos + 1].astype(np.float32), v[:pos + 1])
+            check_cache(st, cache, l, b, h, rows, pos + 1, stats, f"rope step {s} l{l} b{b} h{h}")
+            ref = P.oracle_attention(st, l, h, qpost[l, b, h * G:(h + 1) * G], rows, pos + 1)
+            worst = max(worst, P.rel_err(out[l, b, h * G:(h + 1) * G], ref))
+    log("rope step, max rel err", worst, "stats", vars(stats))
+    assert stats.code_ties <= 1e-4 * stats.codes
+    assert worst <= 2e-3
+
+
+def test_rope_step_graph_replay():
+    """The pre-RoPE step captured once in a graph and replayed for four
+    positions (new inputs and positions copied into the captured buffers
+    between replays, with eager work and synchronizations in between): every
+    replay's output and cache equal an eager run of the same calls on a twin
+    cache, bit for bit (bf16 inputs)."""
+    bg = bgm()
+    base = 1e4
+    st = P.make_setup(13, 2, 1, 2, 4, 256, 128, 2, base, "bf16")
+    L, B, H, G = st.cfg.n_layers, st.cfg.batch, st.cfg.n_kv_heads, st.cfg.group
+    layout, cache_g = build(st)
+    cache_e = bg.Cache(st.cfg)
+    T0 = 100
+    for l in range(L):
+        kvl = [[P.keys_values(st, l, h, 0, T0) for h in range(H)]]
+        append(st, layout, cache_g, l, kvl, [0])
+        append(st, layout, cache_e, l, kvl, [0])
+    rng = np.random.default_rng(5)
+    max_ctx = T0 + 4
+    q_in = torch.zeros((L, B, H * G, 128), dtype=torch.bfloat16, device="cuda")
+    k_in = torch.zeros((L, B, 1, H, 128), dtype=torch.bfloat16, device="cuda")
+    v_in = torch.zeros_like(k_in)
+    pos = torch.zeros(B, dtype=torch.int32, device="cuda")
+    out_g = torch.zeros((L, B, H * G, 128), dtype=torch.float32, device="cuda")
+    ws_g = torch.zeros(bg.rope_step_workspace_bytes(st.cfg, max_ctx), dtype=torch.uint8, device="cuda")
+    ws_e = torch.zeros_like(ws_g)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            bg.blockgtq_rope_decode_step(st.cfg, layout, base, q_in, k_in, v_in, pos, max_ctx, cache_g, out=out_g,
+                                         workspace=ws_g, stream=side)
+    torch.cuda.synchronize()
+    for s in range(4):
+        q = torch.from_numpy(rng.standard_normal((L, B, H * G, 128)).astype(np.float32)).to("cuda", torch.bfloat16)
+        k = torch.from_numpy(rng.standard_normal((L, B, 1, H, 128)).astype(np.float32) * 3).to("cuda", torch.bfloat16)
+        v = torch.from_numpy(rng.standard_normal((L, B, 1, H, 128)).astype(np.float32)).to("cuda", torch.bfloat16)
+        p = torch.tensor([T0 + s], dtype=torch.int32, device="cuda")
+        q_in.copy_(q)
+        k_in.copy_(k)
+        v_in.copy_(v)
+        pos.copy_(p)
+        torch.cuda.synchronize()
+        log("graph replay", s)
+        graph.replay()
+        torch.cuda.synchronize()
+        out_e = bg.blockgtq_rope_decode_step(st.cfg, layout, base, q, k, v, p, max_ctx, cache_e, workspace=ws_e)
+        torch.cuda.synchronize()
+        assert torch.equal(out_g, out_e), f"replay {s}"
+        for name in ("k_codes", "k_norms", "v_codes", "v_norms"):
+            assert torch.equal(getattr(cache_g, name), getattr(cache_e, name)), (s, name)

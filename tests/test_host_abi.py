@@ -157,3 +157,27 @@ def test_window_sizes_and_argument_errors():
     assert app(n_new=0) == 0               # nothing to write
     assert app(ns=0, nr=0) == 0            # no window
     assert app(win=None) == -1
+
+
+def test_rope_step_sizes_and_argument_errors():
+    """Host-side checks of the pre-RoPE decode step (rejected before any launch)."""
+    cfg = bg.Config(n_layers=2, batch=3, n_kv_heads=2, group=4, capacity=1024, k_budget=128, v_bits=2)
+    dec = bg.workspace_bytes(cfg, 2, 0, 1000)
+    a = lambda x: (x + 255) // 256 * 256
+    assert bg.rope_step_workspace_bytes(cfg, 1000) == dec + a(12) + a(2 * 3 * 8 * 512) + 2 * a(2 * 3 * 2 * 512)
+    L = bg.lib()
+    c = cfg.c()
+    fake = ctypes.c_void_p(256)
+    cache = bg._Cache(256, 256, 256, 256)
+
+    def call(base=1e4, max_ctx=1000, ws=10 ** 9, splits=0, q=fake):
+        return L.blockgtq_rope_decode_step(ctypes.byref(c), fake, base, q, fake, fake, fake, max_ctx,
+                                           ctypes.byref(cache), fake, fake, ws, splits, None)
+    assert call(base=1.0) == -1
+    assert call(base=float("inf")) == -1
+    assert call(base=float("nan")) == -1
+    assert call(max_ctx=0) == -3
+    assert call(max_ctx=1025) == -3
+    assert call(splits=5000) == -1
+    assert call(ws=dec) == -4
+    assert call(q=None) == -1
