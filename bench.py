@@ -56,6 +56,8 @@ def parse():
                     help="skip the uniform TQ-MSE K layout (one K group per head) comparison")
     ap.add_argument("--no-protected", action="store_true",
                     help="skip the protected fp16 window (4 sink + 128 recent rows) measurement")
+    ap.add_argument("--no-rope-step", action="store_true",
+                    help="skip the pre-RoPE step measurement (eager and graph-replayed)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one plain device copy of this size first (HBM counter calibration)")
@@ -211,6 +213,53 @@ def protected_measurement(bg, torch, cfg, layout, cache, window, knew_all, vnew_
     return {"n_sink": N_SINK, "n_recent": N_RECENT, "decode_us_median": round(p_us, 2),
             "time_over_no_buffer": round(p_us / dec_med, 3),
             "kernels": "k_window_attn + k_split_mfma (packed rows between the windows)"}
+
+
+def rope_step_measurement(bg, torch, cfg, layout, cache, q_all, knew_all, vnew_all, wps, max_ctx, args, step_med):
+    """The decode step from pre-RoPE inputs (blockgtq_rope_decode_step: RoPE on
+    the device, then the all-layer append and decode), eager and as a captured
+    graph replayed with the position copied into the captured buffer before
+    each replay.  Runs after the main timed loop and rewrites its step rows."""
+    ws = torch.zeros(bg.rope_step_workspace_bytes(cfg, max_ctx, args.n_splits), dtype=torch.uint8, device="cuda")
+    out = torch.empty_like(q_all[0], dtype=torch.float32)
+    n = args.steps
+
+    def eager(s):
+        bg.blockgtq_rope_decode_step(cfg, layout, BASE, q_all[s], knew_all[s], vnew_all[s], wps[s:s + 1], max_ctx,
+                                     cache, out=out, workspace=ws, n_splits=args.n_splits)
+
+    for i in range(args.warmup):
+        eager(args.warmup + i % n)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for i in range(n):
+        ev[i][0].record()
+        eager(args.warmup + i)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    e_us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in ev]))
+    q_in, k_in, v_in = q_all[0].clone(), knew_all[0].clone(), vnew_all[0].clone()
+    pos = wps[args.warmup:args.warmup + 1].clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            bg.blockgtq_rope_decode_step(cfg, layout, BASE, q_in, k_in, v_in, pos, max_ctx, cache, out=out,
+                                         workspace=ws, n_splits=args.n_splits, stream=side)
+    torch.cuda.synchronize()
+    ge = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for i in range(n):
+        s = args.warmup + i
+        ge[i][0].record()
+        pos.copy_(wps[s:s + 1])
+        graph.replay()
+        ge[i][1].record()
+    torch.cuda.synchronize()
+    g_us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in ge]))
+    del graph
+    return {"eager_us_median": round(e_us, 2), "graph_us_median": round(g_us, 2),
+            "graph_over_post_rope_step": round(g_us / step_med, 3),
+            "kernels": "k_rope_step + k_append_rows + k_split_mfma"}
 
 
 def prefill_measurement(bg, synth, torch, bits, sig, rot_k, rot_v, T):
@@ -428,6 +477,10 @@ def main():
         result["protected_window"] = protected_measurement(bg, torch, cfg, layout, cache, window, knew_all, vnew_all,
                                                            wps, q_all, ctxs, max_ctx, args, dec_med)
         del window
+
+    if not args.no_rope_step:
+        result["rope_step"] = rope_step_measurement(bg, torch, cfg, layout, cache, q_all, knew_all, vnew_all, wps,
+                                                    max_ctx, args, float(np.median(step_us)))
 
     if not args.no_prefill:
         result["prefill_attn"] = prefill_measurement(bg, synth, torch, bits, sig, rot_k, rot_v, args.prefill_len)
