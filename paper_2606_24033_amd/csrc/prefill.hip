@@ -33,8 +33,7 @@ typedef float float4_t __attribute__((ext_vector_type(4)));
 constexpr int kThreads = 256;       // rotation kernel: 4 waves
 constexpr int kAttnThreads = 1024;  // attention kernel: 16 waves of 16 query rows
 constexpr int kRows = 256;          // query rows (position x head) per attention workgroup
-constexpr int kQrotPos = 8;          // query positions per rotation chunk (staged together)
-constexpr int kQrotChunks = 16;      // chunks per rotation workgroup (one staging of the rotations)
+constexpr int kQrotRows = 512;       // query rows (position x head) per rotation workgroup
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
 
@@ -102,61 +101,83 @@ __device__ __forceinline__ float ld_q(const void* q, size_t i, int in_dtype) {  
 }
 
 // ---------------------------------------------------------------- 1. rotation
-// grid (ceil(n_q / (kQrotPos kQrotChunks)), n_kv, batch).  qr: [batch][n_q][Hq][128] fp32.
+// grid (ceil(n_q G / kQrotRows), n_kv, batch).  qr: [batch][n_q][Hq][128]
+// fp32.  The rotation of a query row is one product with a 128 x 128 matrix
+// in stream order, W[p][k] = log2 e / sqrt(d_g d_h) Pi_g[j][k - g_pos] for
+// p = g_pos + j and k in the same group g (zero elsewhere), applied to the
+// row gathered into stream order.  W is staged in LDS once per workgroup
+// (transposed, Wt[k][p]); each wave multiplies 16-row tiles by it with fp32
+// MFMAs (16x16x4: 32 steps of 4 coordinates x 8 tiles of 16 outputs).
 __global__ __launch_bounds__(kThreads) void k_prefill_qrot(Dims d, const uint8_t* __restrict__ blob,
                                                            const void* __restrict__ q, int n_q,
                                                            float* __restrict__ qr) {
-  __shared__ float rs[kRowRotFloats];                // the row's group rotations (transposed blocks)
-  __shared__ float qs[(kQrotPos * 8 + 16) * kHeadDim];  // one chunk of queries in stream order (+ rows read, never stored)
-  const int tid = threadIdx.x;
+  __shared__ float wt[kHeadDim * kHeadDim];                  // Wt[k][p]
+  __shared__ float qs[kThreads / 64][16][kHeadDim + 4];      // per wave: 16 rows in stream order
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kvh = blockIdx.y, seq = blockIdx.z;
   const int G = d.group, hq = d.n_kv * G;
   const int n_rows_blob = d.n_layers * d.n_kv;
   const RowMeta* M = reinterpret_cast<const RowMeta*>(blob + kOffRows) + (d.layer * d.n_kv + kvh);
   const float* rowrot = reinterpret_cast<const float*>(blob + layout_rowrot_offset(n_rows_blob)) +
                         static_cast<size_t>(d.layer * d.n_kv + kvh) * kRowRotFloats;
-  const int ng = M->n_groups;
-  int rtot = 0;
-  for (int g = 0; g < ng; ++g) rtot += M->g_dim[g] * M->g_dim[g];
-  for (int i = tid; i < rtot; i += kThreads) rs[i] = rowrot[i];
-  const int p = tid & 127;
-  const int g = M->grp[p], p0 = M->g_pos[g], dg = M->g_dim[g], j = p - p0;
-  const int dimp = M->dim[p];
-  int off = 0;
-  for (int e = 0; e < g; ++e) off += M->g_dim[e] * M->g_dim[e];
-  const float* rt = rs + off;  // Pi_dg transposed: rt[k dg + j] = Pi[j][k]
-  const float scale = kLog2e * rsqrtf(static_cast<float>(dg) * kHeadDim);
-  for (int ch = 0; ch < kQrotChunks; ++ch) {
-    const int i0 = (blockIdx.x * kQrotChunks + ch) * kQrotPos;
-    if (i0 >= n_q) break;  // uniform
-    const int npos = min(kQrotPos, n_q - i0);
-    __syncthreads();  // the previous chunk is consumed (and, first, the rotations are staged)
-    for (int r = tid >> 7; r < npos * G; r += kThreads / kHeadDim) {  // r = position-in-chunk * G + head
-      const int i = i0 + r / G, h = r - (r / G) * G;
-      qs[r * kHeadDim + p] = ld_q(q, ((static_cast<size_t>(seq) * n_q + i) * hq + kvh * G + h) * kHeadDim + dimp,
-                                  d.in_dtype);
-    }
-    __syncthreads();
-    // rows tid >> 7, + 2, + 4, ...: eight at a time, so that one rotation
-    // coefficient feeds eight independent accumulations
-    const int nr = npos * G;
-    for (int r0 = tid >> 7; r0 < nr; r0 += 16) {
-      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      const float* qq = qs + r0 * kHeadDim + p0;  // rows past nr read stale chunk data, never stored
-      for (int k = 0; k < dg; ++k) {
-        const float a = rt[k * dg + j];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) acc[u] = fmaf(a, qq[2 * u * kHeadDim + k], acc[u]);
+  for (int i = tid; i < kHeadDim * kHeadDim; i += kThreads) wt[i] = 0.f;
+  __syncthreads();
+  {
+    // column p (thread & 127) of Wt: the rotation row j = p - g_pos of its group
+    const int p = tid & 127;
+    const int g = M->grp[p], p0 = M->g_pos[g], dg = M->g_dim[g], j = p - p0;
+    int off = 0;
+    for (int e = 0; e < g; ++e) off += M->g_dim[e] * M->g_dim[e];
+    const float scale = kLog2e * rsqrtf(static_cast<float>(dg) * kHeadDim);
+    for (int k = tid >> 7; k < dg; k += kThreads / kHeadDim)
+      wt[(p0 + k) * kHeadDim + p] = rowrot[off + k * dg + j] * scale;  // Pi_dg transposed: [k dg + j] = Pi[j][k]
+  }
+  const int dimk = M->dim[lane], dimk2 = M->dim[lane + 64];  // stream position -> source dim
+  __syncthreads();
+  const int nr = n_q * G;
+  const int r_wg = blockIdx.x * kQrotRows;
+  float (*qw)[kHeadDim + 4] = qs[wave];
+  for (int t0 = r_wg + wave * 16; t0 < min(r_wg + kQrotRows, nr); t0 += kThreads / 4) {
+    // gather 16 rows into stream order (rows past the end are zero)
+    for (int r = 0; r < 16; ++r) {
+      const int row = t0 + r;
+      float a = 0.f, b = 0.f;
+      if (row < nr) {
+        const int i = row / G, h = row - (row / G) * G;
+        const size_t base = ((static_cast<size_t>(seq) * n_q + i) * hq + kvh * G + h) * kHeadDim;
+        a = ld_q(q, base + dimk, d.in_dtype);
+        b = ld_q(q, base + dimk2, d.in_dtype);
       }
+      qw[r][lane] = a;
+      qw[r][lane + 64] = b;
+    }
+    // one wave writes and reads its own rows: LDS operations of a wave
+    // complete in order, so only the compiler must keep the order
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    float4_t acc[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int r = r0 + 2 * u;
-        if (r < nr) {
-          const int i = i0 + r / G, h = r - (r / G) * G;
-          qr[((static_cast<size_t>(seq) * n_q + i) * hq + kvh * G + h) * kHeadDim + p] = acc[u] * scale;
-        }
+    for (int t = 0; t < 8; ++t) acc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
+    const int ar = lane & 15, ak = lane >> 4;
+#pragma unroll 4
+    for (int st = 0; st < kHeadDim / 4; ++st) {
+      const float a = qw[ar][4 * st + ak];
+      const float* wrow = wt + (4 * st + ak) * kHeadDim + ar;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, wrow[16 * t], acc[t], 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = t0 + 4 * ak + i;
+      if (row < nr) {
+        const int qi = row / G, h = row - (row / G) * G;
+        float* dst = qr + ((static_cast<size_t>(seq) * n_q + qi) * hq + kvh * G + h) * kHeadDim + ar;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) dst[16 * t] = acc[t][i];
       }
     }
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");  // reads of these rows before the next tile's writes
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
@@ -424,7 +445,7 @@ hipError_t launch_prefill_attn(const Dims& d, const void* layout, const void* q,
                                float* out, hipStream_t s) {
   using namespace prefill_detail;
   const uint8_t* blob = static_cast<const uint8_t*>(layout);
-  dim3 g1((n_q + kQrotPos * kQrotChunks - 1) / (kQrotPos * kQrotChunks), d.n_kv, d.batch);
+  dim3 g1((n_q * d.group + kQrotRows - 1) / kQrotRows, d.n_kv, d.batch);
   hipLaunchKernelGGL(k_prefill_qrot, g1, dim3(kThreads), 0, s, d, blob, q, n_q, qr_ws);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
