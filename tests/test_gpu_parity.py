@@ -708,3 +708,113 @@ def test_rope_step_graph_replay():
         assert torch.equal(out_g, out_e), f"replay {s}"
         for name in ("k_codes", "k_norms", "v_codes", "v_norms"):
             assert torch.equal(getattr(cache_g, name), getattr(cache_e, name)), (s, name)
+
+
+@pytest.mark.parametrize("T", [262144, 524288])
+def test_qwen_long_context_sampled(T):
+    """Long-context Qwen2.5-3B shape at full size (36 layers, 2 KV heads,
+    G = 8, base 1e6, bf16, K3V3): the context prefilled in 8192-row chunks,
+    then one all-layer append and decode with the split plan for 16 decode
+    steps.  Sampled (layer, KV head) pairs checked in full against the oracle:
+    every code and norm of their T + 1 rows and the attention of their 8
+    query heads."""
+    bg = bgm()
+    L, H, G, chunk = 36, 2, 8, 8192
+    max_ctx = T + 16
+    st = P.make_setup(5, L, 1, H, G, T + 64, 192, 3, 1e6, "bf16", n_cal=2048)
+    layout, cache = build(st)
+    samples = [(4, 1), (35, 0)]
+    kept = {}
+    knew = torch.empty((L, 1, 1, H, 128), dtype=torch.bfloat16, device="cuda")
+    vnew = torch.empty_like(knew)
+    for layer in range(L):
+        sig = np.stack([st.sigma[layer, h] for h in range(H)])
+        k, v = synth.torch_layer_kv(st.seed, layer, T + 1, sig, st.base)
+        for c0 in range(0, T, chunk):
+            bg.blockgtq_quantize_append(st.cfg, layout, layer, k[None, c0:c0 + chunk].contiguous(),
+                                        v[None, c0:c0 + chunk].contiguous(),
+                                        torch.tensor([c0], dtype=torch.int32, device="cuda"), cache)
+        knew[layer, 0, 0] = k[T]
+        vnew[layer, 0, 0] = v[T]
+        for sl, sh in samples:
+            if sl == layer:
+                kept[sl, sh] = (k[:, sh].float().cpu().numpy(), v[:, sh].float().cpu().numpy())
+        del k, v
+    log("qwen long context", T, ": prefill done")
+    q = torch.stack([synth.torch_queries(st.seed, layer, H * G, [T], st.base)[0] for layer in range(L)])[:, None]
+    q = q.contiguous()
+    bg.blockgtq_quantize_append(st.cfg, layout, -1, knew, vnew, torch.tensor([T], dtype=torch.int32, device="cuda"),
+                                cache)
+    out = bg.blockgtq_decode_attn(st.cfg, layout, -1, q, torch.tensor([T + 1], dtype=torch.int32, device="cuda"),
+                                  max_ctx, cache)
+    out = out.cpu().numpy().astype(np.float64)
+    qh = q.float().cpu().numpy()
+    stats = P.Stats()
+    for layer, head in samples:
+        k, v = kept[layer, head]
+        rows = P.oracle_rows(st, layer, head, k, v)
+        check_cache(st, cache, layer, 0, head, rows, T + 1, stats, f"qwen {T} L{layer} h{head}")
+        ref = P.oracle_attention(st, layer, head, qh[layer, 0, head * G:(head + 1) * G], rows, T + 1)
+        err = P.rel_err(out[layer, 0, head * G:(head + 1) * G], ref)
+        log("qwen long context", T, "layer", layer, "head", head, "rel err", err, "ties", vars(stats))
+        assert err <= P.tol_attention()
+    assert stats.code_ties <= 1e-4 * stats.codes
+
+
+def test_ragged_batch8_llama_shape_sampled():
+    """Ragged batched decode at full size: Llama-3.1-8B attention shape (8 KV
+    heads, G = 4, base 5e5, bf16, K3V2; 4 layers), batch 8 with contexts drawn
+    uniformly from [4K, 64K], prefilled by 16384-row quantize_append calls,
+    then one step appending one row per sequence at its own position and one
+    all-layer decode.  Sampled (layer, sequence, KV head) units, the shortest
+    and the longest sequence among them, checked in full against the oracle."""
+    bg = bgm()
+    L, B, H, G, chunk = 4, 8, 8, 4, 16384
+    rng = np.random.default_rng(4)
+    ctx = [int(x) for x in rng.integers(4096, 65536 + 1, size=B)]
+    Tm = max(ctx)
+    st = P.make_setup(4, L, B, H, G, ((Tm + 1 + 63) // 64) * 64, 192, 2, 5e5, "bf16", n_cal=2048)
+    layout, cache = build(st)
+    b_short, b_long = int(np.argmin(ctx)), int(np.argmax(ctx))
+    samples = [(0, b_short, 5), (3, b_long, 2), (2, 3, 7)]
+    kept = {}
+    knew = torch.empty((L, B, 1, H, 128), dtype=torch.bfloat16, device="cuda")
+    vnew = torch.empty_like(knew)
+    for layer in range(L):
+        sig = np.stack([st.sigma[layer, h] for h in range(H)])
+        kv = [synth.torch_layer_kv(st.seed * 16 + b, layer, ctx[b] + 1, sig, st.base) for b in range(B)]
+        for c0 in range(0, Tm, chunk):
+            n = min(chunk, Tm - c0)
+            K = torch.zeros((B, n, H, 128), dtype=torch.bfloat16, device="cuda")
+            V = torch.zeros_like(K)
+            for b in range(B):
+                m = max(0, min(n, ctx[b] - c0))
+                K[b, :m] = kv[b][0][c0:c0 + m]
+                V[b, :m] = kv[b][1][c0:c0 + m]
+            bg.blockgtq_quantize_append(st.cfg, layout, layer, K, V,
+                                        torch.tensor([c0] * B, dtype=torch.int32, device="cuda"), cache)
+        for b in range(B):
+            knew[layer, b, 0] = kv[b][0][ctx[b]]
+            vnew[layer, b, 0] = kv[b][1][ctx[b]]
+        for sl, sb, sh in samples:
+            if sl == layer:
+                kept[sl, sb, sh] = (kv[sb][0][:, sh].float().cpu().numpy(), kv[sb][1][:, sh].float().cpu().numpy())
+        del kv
+    log("ragged batch 8, contexts", ctx, ": prefill done")
+    q = torch.stack([torch.stack([synth.torch_queries(st.seed * 16 + b, layer, H * G, [ctx[b]], st.base)[0]
+                                  for b in range(B)]) for layer in range(L)]).contiguous()
+    wp = torch.tensor(ctx, dtype=torch.int32, device="cuda")
+    bg.blockgtq_quantize_append(st.cfg, layout, -1, knew, vnew, wp, cache, host_write_pos=ctx)
+    out = bg.blockgtq_decode_attn(st.cfg, layout, -1, q, wp + 1, Tm + 1, cache)
+    out = out.cpu().numpy().astype(np.float64)
+    qh = q.float().cpu().numpy()
+    stats = P.Stats()
+    for layer, b, head in samples:
+        k, v = kept[layer, b, head]
+        rows = P.oracle_rows(st, layer, head, k, v)
+        check_cache(st, cache, layer, b, head, rows, ctx[b] + 1, stats, f"ragged L{layer} b{b} h{head}")
+        ref = P.oracle_attention(st, layer, head, qh[layer, b, head * G:(head + 1) * G], rows, ctx[b] + 1)
+        err = P.rel_err(out[layer, b, head * G:(head + 1) * G], ref)
+        log("ragged batch 8 layer", layer, "seq", b, "ctx", ctx[b] + 1, "head", head, "rel err", err)
+        assert err <= P.tol_attention()
+    assert stats.code_ties <= 1e-4 * stats.codes
