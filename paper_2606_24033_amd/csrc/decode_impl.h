@@ -965,9 +965,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     } else {
       load_values<BV>(vn, vw, R, t0, lane);
     }
+    // Wave priorities (the SIMD's issue arbiter prefers the higher one among
+    // its waves): issuing the next tile's loads 3, QK products 2, PV products
+    // 1, softmax 0, so that loads leave early and a wave in its softmax
+    // (transcendentals and cross-lane steps) yields to the product phases
+    // (-4.5 % time in A/B runs against no priorities)
     if (t0 + stride < t_end) {
+      __builtin_amdgcn_s_setprio(3);
       load_keys<KWB>(rw2, knp2, nslot, R, kw, t0 + stride, lane);
       if constexpr (kValuesAhead) load_values<BV>(vn2, vw2, R, t0 + stride, lane);
+      __builtin_amdgcn_s_setprio(0);
     }
     const int tk = t0 + lane;
     {
@@ -985,7 +992,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     float4_t L[NSET];
 #pragma unroll
     for (int s = 0; s < NSET; ++s) L[s] = float4_t{0.f, 0.f, 0.f, 0.f};
+    __builtin_amdgcn_s_setprio(2);
     qk_all<NSET, KWB>(std::make_integer_sequence<int, 8>{}, smem, rw, knp, gmb, rep, lane, L);
+    __builtin_amdgcn_s_setprio(0);
 
     // ---------------- online softmax (lane 4b+i: head i, tokens 4b..4b+3)
     // Logits are in base-2 units (log2 e is folded into the query).  Only a
@@ -1037,7 +1046,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     }
 
     // ---------------- PV: 16 steps of 4 tokens (lane = dim)
+    __builtin_amdgcn_s_setprio(1);
     pv_steps<BV, NSET>(std::make_integer_sequence<int, 16>{}, smem, vw, rep, pp, O);
+    __builtin_amdgcn_s_setprio(0);
   }
 
   finish_unit<NSET>(smem, reinterpret_cast<int*>(smem + kGmeta), d, G, lz, kvh, split, tid, lane, wave, m_run, l_run,
