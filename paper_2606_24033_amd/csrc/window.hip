@@ -19,6 +19,7 @@ namespace bgtq {
 namespace {
 
 constexpr int kWinThreads = 256;
+constexpr int kWinChunk = 136;  // window rows staged per round trip
 constexpr int kMaxWinRows = kMaxSink + kMaxRecent;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInfW = -__builtin_huge_valf();
@@ -67,6 +68,9 @@ __global__ __launch_bounds__(kWinThreads) void k_window_attn(Dims d, const void*
   __shared__ float sc[8][kMaxWinRows];
   __shared__ float ml[8][2];
   __shared__ float red[kWinThreads / 64][8][kHeadDim];
+  __shared__ int slot_of[kMaxWinRows];
+  __shared__ uint4 kst[kWinChunk * 16];  // staged key rows (fp16)
+  __shared__ uint4 vst[kWinChunk * 16];  // staged value rows (fp16)
   const int kvh = blockIdx.x, lz = blockIdx.y;
   const int seq = lz % d.batch;
   const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
@@ -81,30 +85,42 @@ __global__ __launch_bounds__(kWinThreads) void k_window_attn(Dims d, const void*
   for (int i = tid; i < G * kHeadDim; i += kWinThreads)
     qs[i >> 7][i & 127] = ld_in(q, (static_cast<size_t>(lz) * hqn + kvh * G) * kHeadDim + i, d.in_dtype) *
                           (kLog2e * 0.08838834764831845f);  // log2 e / sqrt(d_h)
+  for (int j = tid; j < W; j += kWinThreads) slot_of[j] = win_slot(j < ns ? j : T - nr + (j - ns), n_sink, n_recent);
   __syncthreads();
 
-  // logits: one (window row, head) pair per thread, the key row read as 16
-  // vectors of 8 halves
-  for (int i = tid; i < W * G; i += kWinThreads) {
-    const int j = i / G, g = i - j * G;
-    const int t = j < ns ? j : T - nr + (j - ns);
-    const uint4* kr = reinterpret_cast<const uint4*>(kb + static_cast<size_t>(win_slot(t, n_sink, n_recent)) * kHeadDim);
-    float s = 0.f;
+  // Window rows are staged through LDS in chunks of kWinChunk rows, 16 bytes
+  // per thread and load, so that a chunk costs one memory round trip; the
+  // first value chunk is loaded together with the first key chunk (the
+  // paper's 4 + 128 window is one chunk: one round trip in all).
+  const auto stage = [&](uint4* dst, const _Float16* src, int j0, int n) {
+    for (int i = tid; i < n * 16; i += kWinThreads)
+      dst[i] = reinterpret_cast<const uint4*>(src + static_cast<size_t>(slot_of[j0 + (i >> 4)]) * kHeadDim)[i & 15];
+  };
+  for (int j0 = 0; j0 < W; j0 += kWinChunk) {
+    const int n = min(kWinChunk, W - j0);
+    stage(kst, kb, j0, n);
+    if (j0 == 0) stage(vst, vb, 0, n);
+    __syncthreads();
+    // logits: one (window row, head) pair per thread
+    for (int i = tid; i < n * G; i += kWinThreads) {
+      const int j = i / G, g = i - j * G;
+      float s = 0.f;
 #pragma unroll 4
-    for (int c = 0; c < kHeadDim / 8; ++c) {
-      const uint4 w = kr[c];
-      const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+      for (int c = 0; c < kHeadDim / 8; ++c) {
+        const uint4 w = kst[j * 16 + c];
+        const uint32_t u[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        const _Float16 lo = __builtin_bit_cast(_Float16, static_cast<uint16_t>(u[h] & 0xFFFFu));
-        const _Float16 hi = __builtin_bit_cast(_Float16, static_cast<uint16_t>(u[h] >> 16));
-        s = fmaf(qs[g][8 * c + 2 * h], static_cast<float>(lo), s);
-        s = fmaf(qs[g][8 * c + 2 * h + 1], static_cast<float>(hi), s);
+        for (int h = 0; h < 4; ++h) {
+          const _Float16 lo = __builtin_bit_cast(_Float16, static_cast<uint16_t>(u[h] & 0xFFFFu));
+          const _Float16 hi = __builtin_bit_cast(_Float16, static_cast<uint16_t>(u[h] >> 16));
+          s = fmaf(qs[g][8 * c + 2 * h], static_cast<float>(lo), s);
+          s = fmaf(qs[g][8 * c + 2 * h + 1], static_cast<float>(hi), s);
+        }
       }
+      sc[g][j0 + j] = s;
     }
-    sc[g][j] = s;
+    __syncthreads();
   }
-  __syncthreads();
 
   // softmax per head: one wave per head
   for (int g = wave; g < G; g += kWinThreads / 64) {
@@ -129,24 +145,30 @@ __global__ __launch_bounds__(kWinThreads) void k_window_attn(Dims d, const void*
 
   // sum_j p_j v_j in the original V domain (the packed decode adds it after
   // its output rotation): lane = a pair of dims, wave w takes the rows
-  // j = w mod 4 (one coalesced 256-byte row read per wave and row), then the
-  // four waves' sums are added through LDS
+  // j = w mod 4 of each staged value chunk, then the four waves' sums are
+  // added through LDS
   float2 acc[8];
 #pragma unroll
   for (int g = 0; g < 8; ++g) acc[g] = make_float2(0.f, 0.f);
-#pragma unroll 4
-  for (int j = wave; j < W; j += kWinThreads / 64) {
-    const int t = j < ns ? j : T - nr + (j - ns);
-    const uint32_t vv =
-        *reinterpret_cast<const uint32_t*>(vb + static_cast<size_t>(win_slot(t, n_sink, n_recent)) * kHeadDim + 2 * lane);
-    const float v0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(vv & 0xFFFFu)));
-    const float v1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(vv >> 16)));
+  for (int j0 = 0; j0 < W; j0 += kWinChunk) {
+    const int n = min(kWinChunk, W - j0);
+    if (j0 > 0) {
+      __syncthreads();  // the previous chunk is consumed
+      stage(vst, vb, j0, n);
+      __syncthreads();
+    }
+    const uint32_t* vrow = reinterpret_cast<const uint32_t*>(vst);
+    for (int j = wave; j < n; j += kWinThreads / 64) {
+      const uint32_t vv = vrow[j * (kHeadDim / 2) + lane];
+      const float v0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(vv & 0xFFFFu)));
+      const float v1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(vv >> 16)));
 #pragma unroll
-    for (int g = 0; g < 8; ++g)
-      if (g < G) {
-        acc[g].x = fmaf(sc[g][j], v0, acc[g].x);
-        acc[g].y = fmaf(sc[g][j], v1, acc[g].y);
-      }
+      for (int g = 0; g < 8; ++g)
+        if (g < G) {
+          acc[g].x = fmaf(sc[g][j0 + j], v0, acc[g].x);
+          acc[g].y = fmaf(sc[g][j0 + j], v1, acc[g].y);
+        }
+    }
   }
 #pragma unroll
   for (int g = 0; g < 8; ++g)
