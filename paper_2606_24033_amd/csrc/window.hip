@@ -45,6 +45,7 @@ __global__ __launch_bounds__(kHeadDim) void k_window_append(Dims d, const void* 
   const int seq = lz % d.batch;
   const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
   const int t = write_pos[seq] + i;
+  if (t < 0) return;  // a negative position writes nothing (as in the packed append)
   const bool sink = t < n_sink;
   const bool recent = !sink && n_recent > 0 && i >= n_new - n_recent;
   if (!sink && !recent) return;
