@@ -606,10 +606,12 @@ def _pre_rope(x, pos, base):
 
 
 def test_rope_decode_step_against_oracle():
-    """Decode steps from pre-RoPE inputs (on-device RoPE at position 300..302
-    of a 300-row prefill, fp32 inputs, batch 2, 2 layers, G = 4): the appended
-    codes against the oracle's quantization of its own RoPE of the same
-    pre-RoPE rows (ties counted), the outputs against the oracle within 2e-3."""
+    """Decode steps from pre-RoPE inputs (on-device RoPE; fp32 inputs, batch 2,
+    2 layers, G = 4; a 300-row prefill, then three steps with sequence b at
+    position 300 - 50 b + s, so that the positions and contexts of the batch
+    differ): the appended codes against the oracle's quantization of its own
+    RoPE of the same pre-RoPE rows (ties counted), the outputs against the
+    oracle within 2e-3."""
     bg = bgm()
     base = 5e5
     st = P.make_setup(12, 2, 2, 2, 4, 512, 128, 2, base, "fp32")
@@ -627,12 +629,13 @@ def test_rope_decode_step_against_oracle():
     worst = 0.0
     ws = torch.zeros(bg.rope_step_workspace_bytes(st.cfg, T0 + n_steps), dtype=torch.uint8, device="cuda")
     for s in range(n_steps):
-        pos = T0 + s
+        pos_of = [T0 + s - 50 * b for b in range(B)]
         kpre = np.zeros((L, B, 1, H, 128), np.float32)
         vv = np.zeros((L, B, 1, H, 128), np.float32)
         qpre = np.zeros((L, B, H * G, 128), np.float32)
         qpost = np.zeros((L, B, H * G, 128), np.float64)
         for (l, b, h), (k, v) in kv.items():
+            pos = pos_of[b]
             kpre[l, b, 0, h] = _pre_rope(k[pos], pos, base)
             vv[l, b, 0, h] = v[pos]
             krows[l, b, h][pos] = np.float32(o.rope_absolute(kpre[l, b, 0, h].astype(np.float64), pos, base))
@@ -640,12 +643,13 @@ def test_rope_decode_step_against_oracle():
             qpre[l, b, h * G:(h + 1) * G] = _pre_rope(qp, pos, base)
             qpost[l, b, h * G:(h + 1) * G] = o.rope_absolute(qpre[l, b, h * G:(h + 1) * G].astype(np.float64), pos,
                                                              base)
-        posd = torch.tensor([pos] * B, dtype=torch.int32, device="cuda")
-        log("rope step", s, "position", pos)
+        posd = torch.tensor(pos_of, dtype=torch.int32, device="cuda")
+        log("rope step", s, "positions", pos_of)
         out = bg.blockgtq_rope_decode_step(st.cfg, layout, base, to_dev(qpre, "fp32"), to_dev(kpre, "fp32"),
                                            to_dev(vv, "fp32"), posd, T0 + n_steps, cache, workspace=ws)
         out = out.cpu().numpy().astype(np.float64)
         for (l, b, h), (k, v) in kv.items():
+            pos = pos_of[b]
             rows = P.oracle_rows(st, l, h, krows[l, b, h][:pos + 1].astype(np.float32), v[:pos + 1])
             check_cache(st, cache, l, b, h, rows, pos + 1, stats, f"rope step {s} l{l} b{b} h{h}")
             ref = P.oracle_attention(st, l, h, qpost[l, b, h * G:(h + 1) * G], rows, pos + 1)
