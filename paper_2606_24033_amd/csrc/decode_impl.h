@@ -1161,6 +1161,8 @@ __global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __res
   }
   const int stride = kWaves * 64;
   for (int t0 = t_begin + wave * 64; t0 < t_end; t0 += stride) {
+    // wave priorities as in the packed decode: loads and QK 2, PV 1, softmax 0
+    __builtin_amdgcn_s_setprio(2);
     // every row of the tile is below the capacity (a multiple of 64)
     const uint4* kr = reinterpret_cast<const uint4*>(kb + static_cast<size_t>(t0 + lane) * kHeadDim);
     uint4 ka[4], kn[4];
@@ -1205,6 +1207,7 @@ __global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __res
     f16_qk_chunk<NSET, 24>(std::make_integer_sequence<int, 8>{}, ka, qh, ql, L);
     half4_t vb2[8][2];
     f16_load_values<8>(vb, t0, lane, vb2);
+    __builtin_amdgcn_s_setprio(0);
 
     // ---------------- online softmax, as in the packed decode (value rows
     // past the split end are zeroed: the cache there may hold anything)
@@ -1253,8 +1256,10 @@ __global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __res
     }
 
     // ---------------- PV (lane = dim), 16 steps of 4 tokens
+    __builtin_amdgcn_s_setprio(1);
     f16_pv<NSET, 0>(std::make_integer_sequence<int, 8>{}, va, pp, O);
     f16_pv<NSET, 8>(std::make_integer_sequence<int, 8>{}, vb2, pp, O);
+    __builtin_amdgcn_s_setprio(0);
   }
   __syncthreads();
   finish_unit<NSET>(smem, reinterpret_cast<int*>(smem + kF16Flag), d, G, lz, kvh, split, tid, lane, wave, m_run, l_run,
