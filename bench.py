@@ -247,6 +247,10 @@ def rope_step_measurement(bg, torch, cfg, layout, cache, q_all, knew_all, vnew_a
             bg.blockgtq_rope_decode_step(cfg, layout, BASE, q_in, k_in, v_in, pos, max_ctx, cache, out=out,
                                          workspace=ws, n_splits=args.n_splits, stream=side)
     torch.cuda.synchronize()
+    for i in range(args.warmup):  # the first replays also upload the graph
+        pos.copy_(wps[args.warmup + i % n:args.warmup + i % n + 1])
+        graph.replay()
+    torch.cuda.synchronize()
     ge = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
     for i in range(n):
         s = args.warmup + i
