@@ -18,7 +18,7 @@
 namespace bgtq {
 namespace {
 
-constexpr int kWinThreads = 256;
+constexpr int kWinThreads = 512;
 constexpr int kWinChunk = 136;  // window rows staged per round trip
 constexpr int kMaxWinRows = kMaxSink + kMaxRecent;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -58,7 +58,7 @@ __global__ __launch_bounds__(kHeadDim) void k_window_append(Dims d, const void* 
   base[wcap * kHeadDim + slot] = static_cast<_Float16>(ld_in(v, src, d.in_dtype));
 }
 
-// grid (n_kv, n_lc * batch), 256 threads.  Rows of the window at context T:
+// grid (n_kv, n_lc * batch), 512 threads.  Rows of the window at context T:
 // n_s = min(n_sink, T) sink rows and n_r = min(n_recent, T - n_s) recent rows
 // T - n_r .. T - 1 (the packed decode covers the rows in between).
 __global__ __launch_bounds__(kWinThreads) void k_window_attn(Dims d, const void* __restrict__ q,
@@ -146,7 +146,7 @@ __global__ __launch_bounds__(kWinThreads) void k_window_attn(Dims d, const void*
 
   // sum_j p_j v_j in the original V domain (the packed decode adds it after
   // its output rotation): lane = a pair of dims, wave w takes the rows
-  // j = w mod 4 of each staged value chunk, then the four waves' sums are
+  // j = w mod (waves) of each staged value chunk, then the waves' sums are
   // added through LDS
   float2 acc[8];
 #pragma unroll
@@ -180,7 +180,10 @@ __global__ __launch_bounds__(kWinThreads) void k_window_attn(Dims d, const void*
   __syncthreads();
   for (int i = tid; i < G * kHeadDim; i += kWinThreads) {
     const int g = i >> 7, dd = i & 127;
-    wp[g * 130 + 2 + dd] = (red[0][g][dd] + red[1][g][dd]) + (red[2][g][dd] + red[3][g][dd]);
+    float a = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWinThreads / 64; ++w) a += red[w][g][dd];
+    wp[g * 130 + 2 + dd] = a;
     if (dd == 0) {
       wp[g * 130] = ml[g][0];
       wp[g * 130 + 1] = ml[g][1];
