@@ -178,6 +178,68 @@ def test_closed_forms_and_symmetry():
         assert t[2 ** (b - 1) - 1] == 0.0
 
 
+def _plain_lloyd_gaussian(b, tol=1e-12):
+    """Independent Lloyd-Max solve: plain Lloyd iteration (thresholds at
+    midpoints, centroids at cell means), the cell means taken by 20-point
+    Gauss-Legendre quadrature of the unnormalised density exp(-x^2/2) on each
+    cell (the outer cell cut at 12 beyond its threshold, where the remaining
+    mass is below 1e-31 of it).  Positive half only (the density is even).
+    No Newton step and no closed-form cell probabilities."""
+    xg, wg = np.polynomial.legendre.leggauss(20)
+    n = 1 << b
+    c = np.linspace(0.5, 3.0, n // 2) if n > 2 else np.array([1.0])
+    for _ in range(400000):
+        t = 0.5 * (c[:-1] + c[1:])
+        lo = np.concatenate([[0.0], t])
+        hi = np.concatenate([t, [(t[-1] if len(t) else 0.0) + 12.0]])
+        half, mid = 0.5 * (hi - lo)[:, None], 0.5 * (hi + lo)[:, None]
+        x = half * xg[None, :] + mid
+        w = half * wg[None, :] * np.exp(-0.5 * x * x)
+        cn = (w * x).sum(1) / w.sum(1)
+        step = np.max(np.abs(cn - c))
+        c = cn
+        if step < tol:
+            break
+    return np.concatenate([-c[::-1], c])
+
+
+@pytest.mark.parametrize("b", range(1, 9))
+def test_lloyd_max_equals_plain_lloyd_solve(b):
+    """The oracle's Newton solve of the Lloyd-Max conditions (Sec. 2.2's
+    scalar quantizer, READING Q1) against an independent plain Lloyd iteration
+    on quadrature: centroids agree to 1e-7 for every width used by the cache
+    (the golden table transcribes Max (1960) for b <= 4 only; 5-8 bits are
+    pinned by this solve and by the quadrature check below)."""
+    ref = _plain_lloyd_gaussian(b)
+    got = o.lloyd_max_gaussian(b)
+    assert np.max(np.abs(got - ref)) <= 1e-7
+
+
+@pytest.mark.parametrize("b", range(1, 9))
+def test_lloyd_max_conditions_by_adaptive_quadrature(b):
+    """The two Lloyd-Max conditions checked cell by cell with scipy's adaptive
+    quadrature of the Gaussian density written out (no closed-form moments):
+    each centroid is the conditional mean of its cell between the midpoint
+    thresholds.  The Gaussian is log-concave, so these conditions have one
+    solution (Fleischer 1964): the residual pins the centroids.  The
+    distortion of the oracle's closed form is also re-integrated here, for the
+    fp64 and the fp16-rounded codebook."""
+    from scipy import integrate
+    pdf = lambda x: math.exp(-0.5 * x * x) / math.sqrt(2 * math.pi)
+    c = o.lloyd_max_gaussian(b)
+    t = np.concatenate([[-np.inf], 0.5 * (c[:-1] + c[1:]), [np.inf]])
+    for k in range(len(c)):
+        m0 = integrate.quad(pdf, t[k], t[k + 1], epsabs=0, epsrel=1e-13, limit=200)[0]
+        m1 = integrate.quad(lambda x: x * pdf(x), t[k], t[k + 1], epsabs=0, epsrel=1e-13, limit=200)[0]
+        assert abs(m1 / m0 - c[k]) <= 1e-10 * max(1.0, abs(c[k]))
+    c16, _ = o.codebook(b)
+    for cb in (c, c16):
+        tt = np.concatenate([[-np.inf], 0.5 * (cb[:-1] + cb[1:]), [np.inf]])
+        d = sum(integrate.quad(lambda x, ck=cb[k]: (x - ck) ** 2 * pdf(x), tt[k], tt[k + 1], epsabs=0,
+                               epsrel=1e-12, limit=200)[0] for k in range(len(cb)))
+        assert abs(o.lloyd_max_mse(b, cb) - d) <= 1e-11 * d
+
+
 @pytest.mark.parametrize("b", range(1, 9))
 def test_rate_law(b):
     # E||x - x_hat||^2 <= ||x||^2 sqrt(3) pi / 2 4^-b   (Sec. 2.2), with fp16 centroids
@@ -235,7 +297,13 @@ def test_one_group_is_uniform_tq():
     assert np.all(widths == 3)
 
 
-def test_lemma1_per_block_bound():
+def test_rope_block_logit_error_obeys_block_cauchy_schwarz():
+    """Lemma 1 (App. A.2) as a check of rope_block_logit: the RoPE-logit error
+    of a key perturbation is at most sum_i ||q^(i)|| ||k^(i) - k_hat^(i)||.  The
+    bound holds for any k_hat, so this pins the block rotation structure of
+    rope_block_logit (each block rotated on its own pair of dims by an
+    orthogonal 2x2 map), not the quantizer; a wrong pairing or a scaled
+    rotation in it breaks the bound for some offset."""
     g = np.random.default_rng(12)
     rot_k, _ = synth.rotations(6)
     sig = synth.sigma_profile(6, 0, 0)
@@ -251,6 +319,72 @@ def test_lemma1_per_block_bound():
             err = abs(o.rope_block_logit(q, k[t], delta, 1e4) - o.rope_block_logit(q, kh[t], delta, 1e4))
             bound = sum(np.linalg.norm(o.block(q, i)) * np.linalg.norm(o.block(k[t] - kh[t], i)) for i in range(64))
             assert err <= bound + 1e-12
+    # the bound is tight for a one-block difference aligned with the rotated query block
+    q = np.zeros(128)
+    q[5], q[69] = 3.0, -1.0
+    dk = np.zeros(128)
+    phi = 777 * 1e4 ** (-2.0 * 5 / 128)
+    r = np.array([[math.cos(phi), -math.sin(phi)], [math.sin(phi), math.cos(phi)]])
+    dk[[5, 69]] = r.T @ np.array([3.0, -1.0]) * 0.25
+    err = abs(o.rope_block_logit(q, dk, 777, 1e4))
+    assert abs(err - math.hypot(3.0, 1.0) * np.linalg.norm(dk)) <= 1e-12
+
+
+def test_dequantize_keys_scatter_hand_case():
+    """Same-rate grouping (end of Sec. 3.2) on a hand-built 3-block head
+    (d_h = 6, blocks (0, 3), (1, 4), (2, 5)) with widths [2, 1, 2]: group
+    b = 1 holds block 1 (dims 1, 4), group b = 2 blocks 0 and 2 (dims 0, 3, 2,
+    5), in that stream order.  Rotations are signed permutations, so every
+    expected coordinate is written out by hand from the fp16 centroids:
+    x_hat_g = (n_g / sqrt(d_g)) Pi_g^T C16[codes_g], scattered to the group's
+    dims."""
+    bits = [2, 1, 2]
+    p2 = np.array([[0.0, 1.0], [1.0, 0.0]])                    # swap
+    p4 = np.array([[0.0, 0.0, -1.0, 0.0], [1.0, 0.0, 0.0, 0.0],
+                   [0.0, 0.0, 0.0, 1.0], [0.0, 1.0, 0.0, 0.0]])
+    rot = {2: p2, 4: p4}
+    c1, _ = o.codebook(1)
+    c2, _ = o.codebook(2)
+    # stream codes: [g1: 2 codes][g2: 4 codes]
+    codes = np.array([[0, 1, 3, 0, 2, 1]])
+    norms = np.array([[2.0, 5.0]])                             # radius of g1, of g2
+    got = o.dequantize_keys(codes, norms, bits, rot)
+    # g1: u = (c1[0], c1[1]); Pi^T u swaps -> (c1[1], c1[0]), scale 2 / sqrt(2)
+    # g2: u = (c2[3], c2[0], c2[2], c2[1]); Pi^T u = (u1, u3, -u0, u2), scale 5 / 2
+    want = np.zeros(6)
+    want[1], want[4] = math.sqrt(2.0) * c1[1], math.sqrt(2.0) * c1[0]
+    want[0], want[3], want[2], want[5] = 2.5 * c2[0], 2.5 * c2[1], -2.5 * c2[3], 2.5 * c2[2]
+    np.testing.assert_allclose(got[0], want, rtol=0, atol=1e-15)
+    # the encode side of the same head: stream-order z = sqrt(d_g) Pi_g x_g / ||x_g||
+    x = np.array([[1.0, -2.0, 3.0, 4.0, 0.5, -1.0]])
+    _, widths, kn, z = o.quantize_keys(x, bits, rot)
+    assert list(widths) == [1, 1, 2, 2, 2, 2]
+    np.testing.assert_allclose(kn[0], o.fp16_round([math.hypot(-2.0, 0.5), math.sqrt(1 + 16 + 9 + 1)]))
+    xg2 = np.array([1.0, 4.0, 3.0, -1.0])                       # dims 0, 3, 2, 5
+    want_z = np.concatenate([math.sqrt(2.0) * np.array([0.5, -2.0]) / math.hypot(-2.0, 0.5),
+                             2.0 * np.array([-xg2[2], xg2[0], xg2[3], xg2[1]]) / np.linalg.norm(xg2)])
+    np.testing.assert_allclose(z[0], want_z, rtol=1e-14, atol=1e-15)
+
+
+def test_mixed_group_high_rate_roundtrip():
+    """A mixed schedule of 6-, 7- and 8-bit blocks (three groups, each a
+    different dimension) through quantize_keys / dequantize_keys reproduces
+    the key to the high-rate distortion (Sec. 2.2 rate law at b >= 6: under
+    0.1 % of the energy); a wrong scatter or gather in either direction moves
+    whole coordinates and fails by orders of magnitude."""
+    g = np.random.default_rng(31)
+    rot_k, _ = synth.rotations(4)
+    bits = np.full(64, 7)
+    bits[g.choice(64, 10, replace=False)] = 8
+    bits[np.nonzero(bits == 7)[0][:9]] = 6
+    assert sorted(set(bits.tolist())) == [6, 7, 8]
+    k = g.standard_normal((300, 128)) * np.exp(g.standard_normal(128))[None, :]
+    codes, widths, norms, _ = o.quantize_keys(k, bits, rot_k)
+    assert norms.shape == (300, 3)
+    kh = o.dequantize_keys(codes, norms, bits, rot_k)
+    rel = np.sum((k - kh) ** 2, axis=1) / np.sum(k * k, axis=1)
+    assert np.max(rel) < 1e-3
+    assert np.mean(rel) < math.sqrt(3) * math.pi / 2 * 4.0 ** -6
 
 
 # ------------------------------------------------------------ packing (layout)
