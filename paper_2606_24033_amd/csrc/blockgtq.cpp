@@ -10,7 +10,6 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
-#include <queue>
 #include <string>
 #include <vector>
 
@@ -278,28 +277,37 @@ int blockgtq_allocate(const double* h_scores, int32_t n_rows, int32_t n_blocks, 
   for (long i = 0; i < static_cast<long>(n_rows) * n_blocks; ++i)
     if (!std::isfinite(h_scores[i]) || h_scores[i] < 0.0)
       return fail(BGTQ_EINVAL, "score %ld is negative or not finite", i);
-  struct Item {
-    double key;
-    int idx;
+  // J(b) = sum_i s_i 4^-b_i is separable, and raising block i from b to b + 1
+  // lowers it by (3/4) s_i 4^-b, a gain that shrinks as b grows (Sec. 3.2;
+  // optimality of the greedy rule, App. A.4).  So the optimal schedule takes
+  // the B - L b_min largest of the L (b_max - b_min) candidate gains, each
+  // candidate (block i, level b) being "the bit that takes i from b to b + 1",
+  // and a block's width is b_min plus its number of chosen candidates.  The
+  // gain is ordered by s_i 4^-b (exact: a power-of-two scaling), ties by the
+  // lower block index, then the lower level (which a block takes first).
+  struct Cand {
+    double gain;
+    int block, level;
   };
-  // largest key first; equal keys -> lowest index first
-  auto worse = [](const Item& a, const Item& b) { return a.key < b.key || (a.key == b.key && a.idx > b.idx); };
+  const auto before = [](const Cand& x, const Cand& y) {
+    if (x.gain != y.gain) return x.gain > y.gain;
+    if (x.block != y.block) return x.block < y.block;
+    return x.level < y.level;
+  };
+  const int extra = budget - n_blocks * b_min;
+  std::vector<Cand> cand;
+  cand.reserve(static_cast<size_t>(n_blocks) * (b_max - b_min));
   for (int r = 0; r < n_rows; ++r) {
     const double* s = h_scores + static_cast<size_t>(r) * n_blocks;
     uint8_t* bits = h_bits_out + static_cast<size_t>(r) * n_blocks;
-    std::priority_queue<Item, std::vector<Item>, decltype(worse)> pq(worse);
+    cand.clear();
     for (int i = 0; i < n_blocks; ++i) {
       bits[i] = static_cast<uint8_t>(b_min);
-      // the marginal gain (3/4) s 4^-b is ordered exactly like s 4^-b
-      if (b_min < b_max) pq.push({std::ldexp(s[i], -2 * b_min), i});
+      for (int b = b_min; b < b_max; ++b) cand.push_back({std::ldexp(s[i], -2 * b), i, b});
     }
-    int extra = budget - n_blocks * b_min;
-    while (extra > 0 && !pq.empty()) {
-      Item it = pq.top();
-      pq.pop();
-      int b = ++bits[it.idx];
-      --extra;
-      if (b < b_max) pq.push({std::ldexp(s[it.idx], -2 * b), it.idx});
+    if (extra > 0) {
+      if (extra < static_cast<int>(cand.size())) std::nth_element(cand.begin(), cand.begin() + extra, cand.end(), before);
+      for (int k = 0; k < extra; ++k) ++bits[cand[k].block];
     }
   }
   return ok();

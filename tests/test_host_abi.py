@@ -59,6 +59,27 @@ def test_allocator_small_blocks_and_bounds():
             np.testing.assert_array_equal(bg.blockgtq_allocate(s, B, 2, 4)[0], o.allocate(s, B, 2, 4))
 
 
+def test_allocator_degenerate_scores_vs_oracle():
+    """Scores that stress the tie rules: subnormal and huge values (4^-b
+    scalings that lose bits or underflow to zero), exact power-of-4 ladders
+    (equal gains across blocks at different levels), many zeros, and bounds
+    other than [1, 8]; the library's selection of the largest gains must give
+    the oracle's greedy schedule bit for bit."""
+    g = np.random.default_rng(21)
+    tiny = np.finfo(np.float64).tiny
+    rows = [np.full(64, 5e-324), np.full(64, tiny * 3.0), np.geomspace(5e-324, 1e300, 64),
+            np.array([4.0 ** -(i % 9) for i in range(64)]), np.array([tiny * 4.0 ** (i % 4) for i in range(64)]),
+            np.where(g.random(64) < 0.5, 0.0, np.exp(3 * g.standard_normal(64))),
+            np.repeat([7.0, 7.0 / 4, 7.0 / 16, 7.0 / 64], 16), np.full(64, 1e308)]
+    s = np.stack(rows)
+    for bmin, bmax in ((1, 8), (2, 6), (3, 3), (1, 2)):
+        cands = {64 * bmin, 64 * bmin + 1, 64 * bmin + 37, 32 * (bmin + bmax), 64 * bmax - 1, 64 * bmax}
+        for budget in sorted(b for b in cands if 64 * bmin <= b <= 64 * bmax):
+            got = bg.blockgtq_allocate(s, budget, bmin, bmax)
+            for r in range(len(rows)):
+                np.testing.assert_array_equal(got[r], o.allocate(s[r], budget, bmin, bmax), err_msg=f"row {r} B {budget}")
+
+
 def test_allocator_errors():
     s = np.ones((1, 64))
     with pytest.raises(bg.BlockGTQError) as e:
