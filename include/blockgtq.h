@@ -152,7 +152,10 @@ int blockgtq_layout_init(const bgtq_config* cfg, const uint8_t* h_k_bits,
  * layer in [0, n_layers) or -1 for all layers.
  * d_k, d_v: post-RoPE keys / values in cfg->in_dtype,
  *   [batch][n_new][n_kv_heads][head_dim]  (layer >= 0), or
- *   [n_layers][batch][n_new][n_kv_heads][head_dim]  (layer == -1).
+ *   [n_layers][batch][n_new][n_kv_heads][head_dim]  (layer == -1);
+ *   16-byte aligned (EINVAL otherwise).  Appends of up to 4 rows (decode
+ *   steps) run one latency-oriented kernel; longer ones (prefill) two fp32
+ *   MFMA kernels, keys then values, each a dense 128 x 128 product per row.
  * d_write_pos: int32 [batch]; sequence b's tokens go to rows
  *   d_write_pos[b] .. d_write_pos[b] + n_new - 1.  The caller guarantees
  *   d_write_pos[b] + n_new <= capacity (rows past capacity are not written)
@@ -300,6 +303,14 @@ int blockgtq_rope_decode_step(const bgtq_config* cfg, const void* d_layout, doub
                               const void* d_k_pre, const void* d_v, const int32_t* d_pos, int32_t max_ctx,
                               const bgtq_cache* cache, float* d_out, void* d_workspace, size_t ws_bytes,
                               int32_t n_splits, void* stream);
+
+/* ---- Measurement helper (not a step of the method) ------------------------
+ * Streaming read of d_src[0 .. bytes): the read-bandwidth ceiling that the
+ * decode's roofline fraction is quoted against, next to the nominal 8 TB/s
+ * of HBM3E.  Async on `stream`.  bytes: a positive multiple of 16, d_src
+ * 16-byte aligned (EINVAL otherwise).  d_sink: device uint32[1], written only
+ * when the folded words equal a fixed constant (the loads stay live). */
+int blockgtq_read_probe(const void* d_src, size_t bytes, uint32_t* d_sink, void* stream);
 
 #ifdef __cplusplus
 }

@@ -27,6 +27,7 @@ EXPORTED = [
     "blockgtq_decode_attn_fp16", "blockgtq_prefill_workspace_bytes", "blockgtq_prefill_attn",
     "blockgtq_window_bytes", "blockgtq_window_append", "blockgtq_protected_workspace_bytes",
     "blockgtq_decode_attn_protected", "blockgtq_rope_step_workspace_bytes", "blockgtq_rope_decode_step",
+    "blockgtq_read_probe",
 ]
 
 
@@ -79,6 +80,7 @@ def lib():
             "blockgtq_decode_attn_protected": [P, P, I32, P, P, I32, P, P, I32, I32, P, P, SZ, I32, P],
             "blockgtq_rope_step_workspace_bytes": [P, I32, I32, PSZ],
             "blockgtq_rope_decode_step": [P, P, ctypes.c_double, P, P, P, P, I32, P, P, P, SZ, I32, P],
+            "blockgtq_read_probe": [P, SZ, P, P],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -376,3 +378,10 @@ def blockgtq_rope_decode_step(cfg: Config, layout: Layout, rope_base: float, q_p
                                            _ptr(out), _ptr(workspace), workspace.numel(), n_splits,
                                            _stream(stream)))
     return out
+
+
+def blockgtq_read_probe(src, sink, stream=None):
+    """Stream-read every byte of the device tensor `src` (measurement helper)."""
+    _check_dev(src)
+    _check(lib().blockgtq_read_probe(_ptr(src), src.numel() * src.element_size(), _ptr(sink), _stream(stream)))
+

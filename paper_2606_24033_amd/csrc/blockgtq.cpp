@@ -491,6 +491,23 @@ int blockgtq_layout_init(const bgtq_config* cfg, const uint8_t* h_k_bits, const 
     }
     cost[r] = c;
   }
+  // dense MFMA-order operands of the prefill quantize kernels
+  {
+    float* mv = reinterpret_cast<float*>(blob.data() + layout_rotv_mfma_offset(n_rows));
+    for (int r = 0; r < kHeadDim; ++r)
+      for (int c = 0; c < kHeadDim; ++c) mv[mfma_mat_index(r, c)] = h_rot_v[r * kHeadDim + c];
+    for (int r = 0; r < n_rows; ++r) {
+      const RowMeta& M = rows[r];
+      float* mk = reinterpret_cast<float*>(blob.data() + layout_kdense_offset(n_rows)) +
+                  static_cast<size_t>(r) * kMfmaMatFloats;
+      for (int g = 0; g < M.n_groups; ++g) {
+        const int dg = M.g_dim[g], p0 = M.g_pos[g];
+        const float* pi = h_rot_k + rotk_index(dg);  // row-major Pi_dg
+        for (int j = 0; j < dg; ++j)
+          for (int k = 0; k < dg; ++k) mk[mfma_mat_index(p0 + j, M.dim[p0 + k])] = pi[j * dg + k];
+      }
+    }
+  }
   int32_t* order_all = reinterpret_cast<int32_t*>(blob.data() + layout_order_offset(n_rows));
   int32_t* order_layer = order_all + n_rows;
   const auto by_cost = [&](int a, int b) { return cost[a] > cost[b] || (cost[a] == cost[b] && a < b); };
@@ -524,6 +541,8 @@ int blockgtq_quantize_append(const bgtq_config* cfg, const void* d_layout, int32
   if (n_new > cfg->capacity) return fail(BGTQ_ECAPACITY, "n_new %d > capacity %d", n_new, cfg->capacity);
   if (n_new == 0) return ok();
   if (!d_k || !d_v) return fail(BGTQ_EINVAL, "NULL pointer");
+  if (reinterpret_cast<uintptr_t>(d_k) % 16 != 0 || reinterpret_cast<uintptr_t>(d_v) % 16 != 0)
+    return fail(BGTQ_EINVAL, "k and v must be 16-byte aligned");
   CachePtrs c{static_cast<uint32_t*>(cache->k_codes), static_cast<uint16_t*>(cache->k_norms),
               static_cast<uint32_t*>(cache->v_codes), static_cast<uint16_t*>(cache->v_norms)};
   hipError_t e = launch_quantize_append(dims_of(cfg, layer), d_layout, d_k, d_v, n_new, d_write_pos, c,
@@ -748,6 +767,15 @@ int blockgtq_prefill_attn(const bgtq_config* cfg, const void* d_layout, int32_t 
   hipError_t e = launch_prefill_attn(dims_of(cfg, layer), d_layout, d_q, n_q, d_q_pos0, max_pos, c,
                                      static_cast<float*>(d_workspace), d_out, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "prefill_attn launch");
+  return ok();
+}
+
+int blockgtq_read_probe(const void* d_src, size_t bytes, uint32_t* d_sink, void* stream) {
+  if (!d_src || !d_sink) return fail(BGTQ_EINVAL, "NULL pointer");
+  if (bytes == 0 || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(d_src) % 16 != 0)
+    return fail(BGTQ_EINVAL, "bytes must be a positive multiple of 16 and the source 16-byte aligned");
+  hipError_t e = launch_read_probe(d_src, bytes, d_sink, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "read_probe launch");
   return ok();
 }
 

@@ -22,6 +22,10 @@ struct CachePtrs {
 hipError_t launch_quantize_append(const Dims& d, const void* layout, const void* k,
                                   const void* v, int n_new, const int32_t* write_pos,
                                   const CachePtrs& c, hipStream_t s);
+// The same for appends of more than a few rows (quantize.hip, fp32 MFMAs):
+// k and v 16-byte aligned.
+hipError_t launch_quantize_prefill(const Dims& d, const void* layout, const void* k, const void* v, int n_new,
+                                   const int32_t* write_pos, const CachePtrs& c, hipStream_t s);
 
 // Workspace carve-up of one decode call.
 struct DecodeWs {
@@ -93,5 +97,9 @@ hipError_t launch_decode_fp16(const Dims& d, const void* q, const int32_t* ctx_l
 hipError_t launch_prefill_attn(const Dims& d, const void* layout, const void* q, int n_q,
                                const int32_t* q_pos0, int max_pos, const CachePtrs& c, float* qr_ws,
                                float* out, hipStream_t s);
+
+// Streaming read of `bytes` (a multiple of 16, 16-byte aligned) at src;
+// writes sink[0] only in a case no real input reaches (probe.hip).
+hipError_t launch_read_probe(const void* src, size_t bytes, uint32_t* sink, hipStream_t s);
 
 }  // namespace bgtq

@@ -1,10 +1,10 @@
 // HIP kernels of the Block-GTQ packed-cache path for gfx950 (MI355X).
 //
-//  k_quantize      : TQ-MSE encode (Sec. 2.2) of appended K rows per same-rate
-//                    group (end of Sec. 3.2) and of V rows, dense b-bit pack.
-//  (the packed-cache decode lives in decode_impl.h)
-//  k_append_rows   : the same encode for appends of a few rows (decode steps).
-//  (the fp16 comparator decode lives in decode_impl.h too)
+//  k_append_rows   : TQ-MSE encode (Sec. 2.2) of a few appended K rows per
+//                    same-rate group (end of Sec. 3.2) and of their V rows,
+//                    dense b-bit pack (decode steps).
+//  (long appends run on fp32 MFMAs in quantize.hip; the packed-cache decode
+//  and the fp16 comparator live in decode_impl.h)
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
@@ -40,194 +40,9 @@ __device__ __forceinline__ int scalar_code(const float* thr, int b, float z) {
 }
 
 // ---------------------------------------------------------------------------
-// Quantize + pack + append.  One workgroup per (value tile touched, KV head,
-// sequence[, layer]).  Tokens of the tile outside [write_pos, write_pos+n_new)
-// keep their packed bits.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_quantize(Dims d, const uint8_t* __restrict__ blob,
-                                                  const void* __restrict__ kin,
-                                                  const void* __restrict__ vin, int n_new,
-                                                  const int32_t* __restrict__ wpos, CachePtrs c) {
-  __shared__ float xk[kTile][kHeadDim];
-  __shared__ float xv[kTile][kHeadDim];
-  __shared__ uint8_t ck[kTile][kHeadDim];
-  __shared__ uint8_t cv[kTile][kHeadDim];
-  __shared__ float thr[kThresholdEntries];
-  __shared__ RowMeta meta;
-
-  const int tid = threadIdx.x;
-  const int lz = blockIdx.z;
-  const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
-  const int seq = lz % d.batch;
-  const int head = blockIdx.y;
-  const int wp = wpos[seq];
-  if (wp < 0) return;
-  const int tile = wp / kTile + blockIdx.x;
-  const int t_lo = max(tile * kTile, wp);
-  const int t_hi = min(min(tile * kTile + kTile, wp + n_new), d.capacity);
-  if (t_lo >= t_hi) return;
-
-  const float* gthr = reinterpret_cast<const float*>(blob + kOffThr);
-  const float* rotkt = reinterpret_cast<const float*>(blob + kOffRotKT);
-  const float* rotvt = reinterpret_cast<const float*>(blob + kOffRotVT);
-  const RowMeta* gmeta =
-      reinterpret_cast<const RowMeta*>(blob + kOffRows) + (layer * d.n_kv + head);
-
-  for (int i = tid; i < static_cast<int>(sizeof(RowMeta) / 4); i += 256)
-    reinterpret_cast<uint32_t*>(&meta)[i] = reinterpret_cast<const uint32_t*>(gmeta)[i];
-  for (int i = tid; i < kThresholdEntries; i += 256) thr[i] = gthr[i];
-  const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + head;
-  for (int idx = tid; idx < kTile * kHeadDim; idx += 256) {
-    const int s = idx >> 7, dd = idx & 127;
-    const int t = tile * kTile + s;
-    if (t >= t_lo && t < t_hi) {
-      const size_t off =
-          ((static_cast<size_t>(lz) * n_new + (t - wp)) * d.n_kv + head) * kHeadDim + dd;
-      xk[s][dd] = ld_in(kin, off, d.in_dtype);
-      xv[s][dd] = ld_in(vin, off, d.in_dtype);
-    }
-  }
-  __syncthreads();
-
-  const int wave = tid >> 6, lane = tid & 63;
-  if (t_hi - t_lo <= 4) {
-    // Few tokens (a decode-step append): all four waves work on one token at
-    // a time.  Norms: wave w sums groups w, w+4 and wave 3 the value row, in
-    // the same order as the per-wave path below; rotations: thread p < 128
-    // takes key stream position p, thread 128 + j value coordinate j.  Same
-    // arithmetic as the per-wave path, so the codes are the same.
-    __shared__ float gnrm[kMaxGroups + 1];
-    const int ng = meta.n_groups;
-    for (int t = t_lo; t < t_hi; ++t) {
-      const int s = t - tile * kTile;
-      for (int g = wave; g < ng; g += 4) {
-        const int dg = meta.g_dim[g], p0 = meta.g_pos[g];
-        float ss = 0.f;
-        for (int i = lane; i < dg; i += 64) {
-          const float x = xk[s][meta.dim[p0 + i]];
-          ss = fmaf(x, x, ss);
-        }
-        ss = wave_sum(ss);
-        if (lane == 0) gnrm[g] = sqrtf(ss);
-      }
-      if (wave == 3) {
-        float ss = 0.f;
-        for (int i = lane; i < kHeadDim; i += 64) ss = fmaf(xv[s][i], xv[s][i], ss);
-        ss = wave_sum(ss);
-        if (lane == 0) gnrm[kMaxGroups] = sqrtf(ss);
-      }
-      __syncthreads();
-      if (tid < kHeadDim) {
-        const int p = tid, g = meta.grp[p];
-        const int b = meta.g_bits[g], dg = meta.g_dim[g], p0 = meta.g_pos[g], j = p - p0;
-        const float nrm = gnrm[g];
-        const float scale = nrm > 0.f ? sqrtf(static_cast<float>(dg)) / nrm : 0.f;
-        const float* rt = rotkt + rotk_index(dg);
-        float acc = 0.f;
-#pragma unroll 16
-        for (int i = 0; i < dg; ++i) acc = fmaf(rt[i * dg + j], xk[s][meta.dim[p0 + i]], acc);
-        ck[s][p] = static_cast<uint8_t>(scalar_code(thr + thr_index(b), b, acc * scale));
-        if (j == 0) c.k_norms[row * kMaxGroups * d.capacity + t * ((ng + 1) & ~1) + g] = __half_as_ushort(__float2half_rn(nrm));
-      } else {
-        const int j = tid - kHeadDim, b = d.v_bits;
-        const float nrm = gnrm[kMaxGroups];
-        const float scale = nrm > 0.f ? sqrtf(static_cast<float>(kHeadDim)) / nrm : 0.f;
-        float acc = 0.f;
-#pragma unroll 16
-        for (int i = 0; i < kHeadDim; ++i) acc = fmaf(rotvt[i * kHeadDim + j], xv[s][i], acc);
-        cv[s][j] = static_cast<uint8_t>(scalar_code(thr + thr_index(b), b, acc * scale));
-        if (j == 0) c.v_norms[row * d.capacity + t] = __half_as_ushort(__float2half_rn(nrm));
-      }
-      __syncthreads();
-    }
-  }
-  for (int s = wave; s < kTile && t_hi - t_lo > 4; s += 4) {
-    const int t = tile * kTile + s;
-    if (t < t_lo || t >= t_hi) continue;
-    for (int g = 0; g < meta.n_groups; ++g) {
-      const int b = meta.g_bits[g], dg = meta.g_dim[g], p0 = meta.g_pos[g];
-      float ss = 0.f;
-      for (int i = lane; i < dg; i += 64) {
-        const float x = xk[s][meta.dim[p0 + i]];
-        ss = fmaf(x, x, ss);
-      }
-      ss = wave_sum(ss);
-      const float nrm = sqrtf(ss);
-      const float scale = nrm > 0.f ? sqrtf(static_cast<float>(dg)) / nrm : 0.f;
-      const float* rt = rotkt + rotk_index(dg);
-      for (int j = lane; j < dg; j += 64) {
-        float acc = 0.f;
-        for (int i = 0; i < dg; ++i) acc = fmaf(rt[i * dg + j], xk[s][meta.dim[p0 + i]], acc);
-        ck[s][p0 + j] = static_cast<uint8_t>(scalar_code(thr + thr_index(b), b, acc * scale));
-      }
-      if (lane == 0)
-        c.k_norms[row * kMaxGroups * d.capacity + t * ((meta.n_groups + 1) & ~1) + g] =
-            __half_as_ushort(__float2half_rn(nrm));
-    }
-    {
-      const int b = d.v_bits;
-      float ss = 0.f;
-      for (int i = lane; i < kHeadDim; i += 64) ss = fmaf(xv[s][i], xv[s][i], ss);
-      ss = wave_sum(ss);
-      const float nrm = sqrtf(ss);
-      const float scale = nrm > 0.f ? sqrtf(static_cast<float>(kHeadDim)) / nrm : 0.f;
-      for (int j = lane; j < kHeadDim; j += 64) {
-        float acc = 0.f;
-        for (int i = 0; i < kHeadDim; ++i) acc = fmaf(rotvt[i * kHeadDim + j], xv[s][i], acc);
-        cv[s][j] = static_cast<uint8_t>(scalar_code(thr + thr_index(b), b, acc * scale));
-      }
-      if (lane == 0) c.v_norms[row * d.capacity + t] = __half_as_ushort(__float2half_rn(nrm));
-    }
-  }
-  __syncthreads();
-
-  // key rows: word w of a row collects every code whose bits meet [32w, 32w+32)
-  const int kw = d.k_words;
-  for (int idx = tid; idx < kTile * kw; idx += 256) {
-    const int s = idx / kw, w = idx - s * kw;
-    const int t = tile * kTile + s;
-    if (t < t_lo || t >= t_hi) continue;
-    uint32_t word = 0;
-    for (int p = meta.word_first[w]; p < kHeadDim; ++p) {
-      const int rel = static_cast<int>(meta.bitoff[p]) - 32 * w;
-      if (rel >= 32) break;
-      const uint32_t code = ck[s][p];
-      word |= rel >= 0 ? (code << rel) : (code >> (-rel));
-    }
-    c.k_codes[(row * d.capacity + t) * kw + w] = word;
-  }
-  // value tile: word w of coordinate j holds slots whose bits meet [32w, 32w+32)
-  const int bv = d.v_bits;
-  const uint64_t fmask = (1ull << bv) - 1;
-  for (int idx = tid; idx < kHeadDim * bv; idx += 256) {
-    const int j = idx / bv, w = idx - j * bv;
-    const size_t addr =
-        ((row * (d.capacity / kTile) + tile) * kHeadDim + j) * static_cast<size_t>(bv) + w;
-    uint32_t word = c.v_codes[addr];
-    for (int s = 0; s < kTile; ++s) {
-      const int t = tile * kTile + s;
-      if (t < t_lo || t >= t_hi) continue;
-      const int rel = s * bv - 32 * w;
-      if (rel <= -bv || rel >= 32) continue;
-      const uint64_t code = cv[s][j];
-      uint32_t m, v;
-      if (rel >= 0) {
-        m = static_cast<uint32_t>(fmask << rel);
-        v = static_cast<uint32_t>(code << rel);
-      } else {
-        m = static_cast<uint32_t>(fmask >> (-rel));
-        v = static_cast<uint32_t>(code >> (-rel));
-      }
-      word = (word & ~m) | (v & m);
-    }
-    c.v_codes[addr] = word;
-  }
-}
-
-// ---------------------------------------------------------------------------
 // Decode-step append: n_new <= kRowAppend rows per (KV head, sequence[,
-// layer]), one 1024-thread workgroup each.  Same encode as k_quantize
-// (Sec. 2.2 per same-rate group, and the value row), arranged for latency:
+// layer]), one 1024-thread workgroup each.  The encode of Sec. 2.2 per
+// same-rate group, and of the value row, arranged for latency:
 // every global read is issued in one round, each thread's 32 rotation
 // coefficients in flight together and used for all the rows.  Threads
 // [0, 512): key stream position p = tid % 128 and summation quarter tid / 128
@@ -442,10 +257,7 @@ hipError_t launch_quantize_append(const Dims& d, const void* layout, const void*
                        static_cast<const uint8_t*>(layout), k, v, n_new, write_pos, c);
     return hipGetLastError();
   }
-  dim3 grid((n_new + kTile - 1) / kTile + 1, d.n_kv, d.batch * d.n_lc);
-  hipLaunchKernelGGL(k_quantize, grid, dim3(256), 0, s, d, static_cast<const uint8_t*>(layout), k,
-                     v, n_new, write_pos, c);
-  return hipGetLastError();
+  return launch_quantize_prefill(d, layout, k, v, n_new, write_pos, c, s);
 }
 
 hipError_t launch_decode_packed(const Dims& d, const void* layout, const void* q,

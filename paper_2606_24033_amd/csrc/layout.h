@@ -105,8 +105,30 @@ __host__ __device__ constexpr uint64_t layout_order_offset(int n_rows) {
 __host__ __device__ constexpr uint64_t layout_rowrot_offset(int n_rows) {
   return align256(layout_order_offset(n_rows) + 8ull * static_cast<uint64_t>(n_rows));
 }
+// Then the operands of the prefill quantize kernels (quantize.hip), in the
+// order the fp32 16x16x4 MFMAs read them: matrix M (128 x 128) is stored as
+// [t][s4][lane][e] = M[16 t + lane % 16][32 (lane / 16) + 4 s4 + e], so that
+// lane l's float4 at ((t * 8 + s4) * 64 + l) is its operand for the four
+// k-steps 4 s4 .. 4 s4 + 3 of output tile t (k-step s of lane l pairs with
+// input dim 32 (l / 16) + s):
+//  * once: Pi_V;
+//  * per row: its key rotation on the input's natural dims, W[p][d] =
+//    Pi_g[j][k] for stream position p = g_pos + j and dim d = dim[g_pos + k]
+//    of the same group g, zero elsewhere (the gather into stream order is
+//    folded into the matrix).
+constexpr int kMfmaMatFloats = kHeadDim * kHeadDim;
+__host__ __device__ constexpr uint64_t layout_rotv_mfma_offset(int n_rows) {
+  return align256(layout_rowrot_offset(n_rows) + 4ull * kRowRotFloats * static_cast<uint64_t>(n_rows));
+}
+__host__ __device__ constexpr uint64_t layout_kdense_offset(int n_rows) {
+  return layout_rotv_mfma_offset(n_rows) + 4ull * kMfmaMatFloats;
+}
 __host__ __device__ constexpr uint64_t layout_total_bytes(int n_rows) {
-  return layout_rowrot_offset(n_rows) + 4ull * kRowRotFloats * static_cast<uint64_t>(n_rows);
+  return layout_kdense_offset(n_rows) + 4ull * kMfmaMatFloats * static_cast<uint64_t>(n_rows);
+}
+// index of M[r][c] in the MFMA operand order above
+__host__ __device__ constexpr int mfma_mat_index(int r, int c) {
+  return (((r >> 4) * 8 + ((c & 31) >> 2)) * 64 + (c >> 5) * 16 + (r & 15)) * 4 + (c & 3);
 }
 
 }  // namespace bgtq

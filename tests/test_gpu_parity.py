@@ -367,6 +367,47 @@ def test_small_appends_cross_tiles_and_value_words():
     assert stats.code_ties <= 1e-4 * stats.codes
 
 
+@pytest.mark.parametrize("k_budget,v_bits,dtype", [(64, 1, "bf16"), (160, 3, "bf16"), (192, 5, "fp32"),
+                                                    (320, 8, "bf16"), (512, 7, "fp32"), (100, 4, "bf16")])
+def test_prefill_append_kernels_widths_and_offsets(k_budget, v_bits, dtype):
+    """The long-append encode (quantize.hip, fp32 MFMAs): appends of 5, 17,
+    33, 1100 and 6 rows per call at positions that start inside value tiles
+    (3 and 31), so that consecutive calls share tiles and every tile edge
+    case (a call ending or starting mid-tile, a call inside one tile) occurs;
+    key rows of 4 to 32 words, value widths 1-8, bf16 and fp32 inputs, two
+    layers x 2 sequences x 2 KV heads.  Every code and radius of every row
+    against the oracle, bit-exact up to counted ties."""
+    st = P.make_setup(50 + v_bits, 2, 2, 2, 4, 1280, k_budget, v_bits, 5e5, dtype)
+    layout, cache = build(st)
+    sizes = [5, 17, 33, 1100, 6]
+    starts = [3, 31]
+    total = sum(sizes)
+    kv = {(l, b, h): P.keys_values(st, l, h, 777 * b, starts[b] + total) for l in range(2) for b in range(2)
+          for h in range(2)}
+    junk = {(l, h): P.keys_values(st, l, h, 99999, 31) for l in range(2) for h in range(2)}
+    for layer in range(2):
+        # one 31-row call: real rows below each sequence's start, other rows
+        # above it (overwritten by the appends that follow)
+        pre = [[(np.concatenate([kv[layer, b, h][0][:starts[b]], junk[layer, h][0][starts[b]:]]),
+                 np.concatenate([kv[layer, b, h][1][:starts[b]], junk[layer, h][1][starts[b]:]])) for h in range(2)]
+               for b in range(2)]
+        append(st, layout, cache, layer, pre, [0, 0])
+    pos = list(starts)
+    for n in sizes:
+        for layer in range(2):
+            kvb = [[(kv[layer, b, h][0][pos[b]:pos[b] + n], kv[layer, b, h][1][pos[b]:pos[b] + n]) for h in range(2)]
+                   for b in range(2)]
+            append(st, layout, cache, layer, kvb, pos)
+        pos = [p + n for p in pos]
+    stats = P.Stats()
+    for (l, b, h), (k, v) in kv.items():
+        n = pos[b]
+        rows = P.oracle_rows(st, l, h, k[:n], v[:n])
+        check_cache(st, cache, l, b, h, rows, n, stats, f"prefill kernels K{k_budget}V{v_bits} l{l} b{b} h{h}")
+    log(f"prefill kernels K{k_budget} V{v_bits} {dtype}: ties {vars(stats)}")
+    assert stats.code_ties <= 1e-4 * stats.codes
+
+
 def test_fp16_comparator_group8_ragged_and_poisoned_tail():
     """The fp16 comparator decode (MFMA kernel) with G = 8 query heads per KV
     head, ragged contexts that end inside a tile, several splits, and NaN in
@@ -492,19 +533,77 @@ def test_argument_errors_on_device():
         bg.Layout(st.cfg, bad, synth.flat_rot_k(st.rot_k), st.rot_v)
 
 
-def test_llama_128k_step_sampled():
+@pytest.mark.parametrize("G,v_bits,k_budget", [(1, 5, 192), (2, 6, 256), (3, 7, 128), (5, 5, 192), (6, 6, 160),
+                                                (7, 7, 224), (3, 1, 64), (6, 4, 320)])
+def test_decode_query_groups_and_value_widths(G, v_bits, k_budget):
+    """Decode attention (Sec. 4) for GQA groups of 1-7 query heads (a partial
+    first set of four heads for G < 4; a partial second set for G = 5..7) and
+    value widths 1 and 4-7, over key rows of 8, 10, 12, 16 and 20 words:
+    2 layers x batch 2 x 2 KV heads, bf16, contexts 1300 and 77 rows,
+    all-layer calls with 0, 1 and 3 splits and single-layer calls that must
+    give the same bits at 1 and 3 splits.  Codes and radii
+    bit-exact up to counted ties, attention within 2e-3 of the oracle, and the
+    fp16 comparator on the same group within 2e-3 of the definition on fp16
+    rows."""
+    bg = bgm()
+    lens = [1300, 77]
+    st = P.make_setup(40 + G, 2, 2, 2, G, 1344, k_budget, v_bits, 5e5, "bf16")
+    L, B, H = 2, 2, 2
+    layout, cache = build(st)
+    kv = {(l, b, h): P.keys_values(st, l, h, 5000 * b, lens[b]) for l in range(L) for b in range(B) for h in range(H)}
+    for l in range(L):
+        pre = [[(np.concatenate([kv[l, b, h][0], kv[l, 0, h][0][:lens[0] - lens[b]]]),
+                 np.concatenate([kv[l, b, h][1], kv[l, 0, h][1][:lens[0] - lens[b]]])) for h in range(H)]
+               for b in range(B)]
+        append(st, layout, cache, l, pre, [0, 0])
+    rows = {key: P.oracle_rows(st, key[0], key[2], *kv[key]) for key in kv}
+    stats = P.Stats()
+    for (l, b, h), r in rows.items():
+        check_cache(st, cache, l, b, h, r, lens[b], stats, f"G{G} bv{v_bits} L{l} b{b} h{h}")
+    qs = np.stack([np.stack([np.concatenate([synth.cast(synth.queries(st.seed, l, h, lens[b] - 1, G, st.base, step=b),
+                                                        "bf16") for h in range(H)]) for b in range(B)])
+                   for l in range(L)])                                   # [L, B, H G, 128]
+    ctx = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    refs = {(l, b, h): P.oracle_attention(st, l, h, qs[l, b, h * G:(h + 1) * G], rows[l, b, h], lens[b])
+            for (l, b, h) in rows}
+    for ns in (0, 1, 3):
+        out = bg.blockgtq_decode_attn(st.cfg, layout, -1, to_dev(qs, "bf16"), ctx, max(lens), cache, n_splits=ns)
+        out = out.cpu().numpy().astype(np.float64)
+        for (l, b, h), ref in refs.items():
+            err = P.rel_err(out[l, b, h * G:(h + 1) * G], ref)
+            assert err <= P.tol_attention(), (ns, l, b, h, err)
+        if ns > 0:  # same split plan: the single-layer call gives the same bits
+            one = bg.blockgtq_decode_attn(st.cfg, layout, 1, to_dev(qs[1], "bf16"), ctx, max(lens), cache,
+                                          n_splits=ns)
+            np.testing.assert_array_equal(one.cpu().numpy(), out[1].astype(np.float32))
+    log(f"G {G} v_bits {v_bits} k_budget {k_budget}: attention ok, ties {vars(stats)}")
+    k16 = torch.zeros((L, B, H, st.cfg.capacity, 128), dtype=torch.float16, device="cuda")
+    v16 = torch.zeros_like(k16)
+    for (l, b, h), (k, v) in kv.items():
+        k16[l, b, h, :lens[b]] = torch.from_numpy(k.astype(np.float32)).half().cuda()
+        v16[l, b, h, :lens[b]] = torch.from_numpy(v.astype(np.float32)).half().cuda()
+    out16 = bg.blockgtq_decode_attn_fp16(st.cfg, -1, to_dev(qs, "bf16"), ctx, max(lens), k16, v16, n_splits=2)
+    out16 = out16.cpu().numpy().astype(np.float64)
+    for (l, b, h), (k, v) in kv.items():
+        ref16 = o.attention(qs[l, b, h * G:(h + 1) * G], k.astype(np.float16).astype(np.float64),
+                            v.astype(np.float16).astype(np.float64))
+        assert P.rel_err(out16[l, b, h * G:(h + 1) * G], ref16) <= P.tol_attention()
+    assert stats.code_ties <= 1e-4 * stats.codes
+
+
+@pytest.fixture(scope="module")
+def llama_128k():
     """Full-size step in the launch configuration bench.py times: Llama-3.1-8B
     shape (32 layers, 8 KV heads, G = 4, base 5e5, bf16, K2V2), 131072 cached
     rows, one all-layer append of row 131072 and one all-layer decode with the
-    default split plan for bench.py's max_ctx.  Sampled (layer, KV head) pairs
-    are checked in full against the oracle fed the same bf16 inputs: every
-    code and norm of their 131073 rows and the attention of their 4 query heads."""
+    default split plan for bench.py's max_ctx.  Keeps the inputs of two whole
+    layers for the oracle."""
     bg = bgm()
     T, L, H, G = 131072, 32, 8, 4
     max_ctx = T + 25                    # bench.py default: 5 warm-up + 20 timed steps
     st = P.make_setup(3, L, 1, H, G, T + 64, 128, 2, 5e5, "bf16", n_cal=2048)
     layout, cache = build(st)
-    samples = [(5, 3), (27, 6)]
+    kept_layers = (5, 27)
     kept = {}
     knew = torch.empty((L, 1, 1, H, 128), dtype=torch.bfloat16, device="cuda")
     vnew = torch.empty_like(knew)
@@ -516,9 +615,8 @@ def test_llama_128k_step_sampled():
                                     cache)
         knew[layer, 0, 0] = k[T]
         vnew[layer, 0, 0] = v[T]
-        for sl, sh in samples:
-            if sl == layer:
-                kept[sl, sh] = (k[:, sh].float().cpu().numpy(), v[:, sh].float().cpu().numpy())
+        if layer in kept_layers:
+            kept[layer] = (k.float().cpu().numpy(), v.float().cpu().numpy())
         del k, v
     log("llama 128k: prefill done")
     q = torch.stack([synth.torch_queries(st.seed, layer, H * G, [T], st.base)[0] for layer in range(L)])[:, None]
@@ -528,16 +626,28 @@ def test_llama_128k_step_sampled():
     out = bg.blockgtq_decode_attn(st.cfg, layout, -1, q, torch.tensor([T + 1], dtype=torch.int32, device="cuda"),
                                   max_ctx, cache)
     out = out.cpu().numpy().astype(np.float64)
-    qh = q.float().cpu().numpy()
+    yield dict(st=st, cache=cache, out=out, qh=q.float().cpu().numpy(), kept=kept, T=T, H=H, G=G)
+    del layout, cache
+
+
+@pytest.mark.parametrize("layer", [5, 27])
+def test_llama_128k_step_whole_layer(llama_128k, layer):
+    """Every KV head of one layer of the 128K Llama-shaped step checked in full
+    against the oracle fed the same bf16 inputs: every code and norm of its
+    131073 rows and the attention of all 32 query heads of the layer."""
+    d = llama_128k
+    st, T, H, G = d["st"], d["T"], d["H"], d["G"]
+    k_all, v_all = d["kept"][layer]
     stats = P.Stats()
-    for layer, head in samples:
-        k, v = kept[layer, head]
-        rows = P.oracle_rows(st, layer, head, k, v)
-        check_cache(st, cache, layer, 0, head, rows, T + 1, stats, f"llama L{layer} h{head}")
-        ref = P.oracle_attention(st, layer, head, qh[layer, 0, head * G:(head + 1) * G], rows, T + 1)
-        err = P.rel_err(out[layer, 0, head * G:(head + 1) * G], ref)
-        log("llama 128k layer", layer, "head", head, "rel err", err, "ties", vars(stats))
-        assert err <= P.tol_attention()
+    worst = 0.0
+    for head in range(H):
+        rows = P.oracle_rows(st, layer, head, k_all[:, head], v_all[:, head])
+        check_cache(st, d["cache"], layer, 0, head, rows, T + 1, stats, f"llama L{layer} h{head}")
+        ref = P.oracle_attention(st, layer, head, d["qh"][layer, 0, head * G:(head + 1) * G], rows, T + 1)
+        err = P.rel_err(d["out"][layer, 0, head * G:(head + 1) * G], ref)
+        worst = max(worst, err)
+        assert err <= P.tol_attention(), (head, err)
+    log("llama 128k layer", layer, "all heads, worst rel err", worst, "ties", vars(stats))
     assert stats.code_ties <= 1e-4 * stats.codes
 
 
@@ -719,15 +829,16 @@ def test_qwen_long_context_sampled(T):
     """Long-context Qwen2.5-3B shape at full size (36 layers, 2 KV heads,
     G = 8, base 1e6, bf16, K3V3): the context prefilled in 8192-row chunks,
     then one all-layer append and decode with the split plan for 16 decode
-    steps.  Sampled (layer, KV head) pairs checked in full against the oracle:
-    every code and norm of their T + 1 rows and the attention of their 8
-    query heads."""
+    steps.  Whole layers (both KV heads: two layers at 256K rows, one at 512K)
+    checked in full against the oracle: every code and norm of their T + 1
+    rows and the attention of their 16 query heads."""
     bg = bgm()
     L, H, G, chunk = 36, 2, 8, 8192
     max_ctx = T + 16
     st = P.make_setup(5, L, 1, H, G, T + 64, 192, 3, 1e6, "bf16", n_cal=2048)
     layout, cache = build(st)
-    samples = [(4, 1), (35, 0)]
+    # whole layers: both KV heads of layers 4 and 35 at 256K, of layer 35 at 512K
+    samples = [(4, 0), (4, 1), (35, 0), (35, 1)] if T <= 262144 else [(35, 0), (35, 1)]
     kept = {}
     knew = torch.empty((L, 1, 1, H, 128), dtype=torch.bfloat16, device="cuda")
     vnew = torch.empty_like(knew)
