@@ -304,6 +304,25 @@ int blockgtq_rope_decode_step(const bgtq_config* cfg, const void* d_layout, doub
                               const bgtq_cache* cache, float* d_out, void* d_workspace, size_t ws_bytes,
                               int32_t n_splits, void* stream);
 
+/* ---- Decode attention that allocates nothing ---------------------------------
+ * For callers that cannot allocate device memory or pass a workspace: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same computation, arguments and results as
+ * blockgtq_decode_attn (bit-identical for the same n_splits), except that
+ * the split counters and partials live in a static device array of
+ * BGTQ_NOALLOC_SCRATCH_BYTES bytes per GPU (held until the process ends; its
+ * address is looked up on the first call on each device).  Two launches on
+ * `stream`: a fill kernel that zeroes the counters, then the decode.  A
+ * call whose workspace (blockgtq_workspace_bytes for the same arguments)
+ * exceeds the array fails with BGTQ_EWORKSPACE before anything is enqueued.
+ * No hipMalloc / hipFree or allocating library call is made.  Calls that
+ * overlap in time on one GPU share the array and race: the caller serialises
+ * them (one stream, or events). */
+#define BGTQ_NOALLOC_SCRATCH_BYTES (8u << 20)
+int blockgtq_decode_attn_noalloc(const bgtq_config* cfg, const void* d_layout, int32_t layer, const void* d_q,
+                                 const int32_t* d_ctx_len, int32_t max_ctx, const bgtq_cache* cache, float* d_out,
+                                 int32_t n_splits, void* stream);
+
 /* ---- Measurement helper (not a step of the method) ------------------------
  * Streaming read of d_src[0 .. bytes): the read-bandwidth ceiling that the
  * decode's roofline fraction is quoted against, next to the nominal 8 TB/s

@@ -27,7 +27,7 @@ EXPORTED = [
     "blockgtq_decode_attn_fp16", "blockgtq_prefill_workspace_bytes", "blockgtq_prefill_attn",
     "blockgtq_window_bytes", "blockgtq_window_append", "blockgtq_protected_workspace_bytes",
     "blockgtq_decode_attn_protected", "blockgtq_rope_step_workspace_bytes", "blockgtq_rope_decode_step",
-    "blockgtq_read_probe",
+    "blockgtq_read_probe", "blockgtq_decode_attn_noalloc",
 ]
 
 
@@ -81,6 +81,7 @@ def lib():
             "blockgtq_rope_step_workspace_bytes": [P, I32, I32, PSZ],
             "blockgtq_rope_decode_step": [P, P, ctypes.c_double, P, P, P, P, I32, P, P, P, SZ, I32, P],
             "blockgtq_read_probe": [P, SZ, P, P],
+            "blockgtq_decode_attn_noalloc": [P, P, I32, P, P, I32, P, P, I32, P],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -254,6 +255,20 @@ def blockgtq_decode_attn(cfg: Config, layout: Layout, layer: int, q, ctx_len, ma
     _check(lib().blockgtq_decode_attn(ctypes.byref(cfg.c()), _ptr(layout.blob), layer, _ptr(q), _ptr(ctx_len),
                                       max_ctx, ctypes.byref(cache.c()), _ptr(out), _ptr(workspace),
                                       workspace.numel(), n_splits, _stream(stream)))
+    return out
+
+
+def blockgtq_decode_attn_noalloc(cfg: Config, layout: Layout, layer: int, q, ctx_len, max_ctx: int, cache: Cache,
+                                 out, n_splits: int = 0, stream=None):
+    """blockgtq_decode_attn with its workspace in the library's static device
+    array (no allocation in the call; `out` is the caller's)."""
+    import torch
+    _check_dev(q, _in_dtype(cfg))
+    _check_dev(ctx_len, torch.int32)
+    _check_dev(out, torch.float32)
+    _check(lib().blockgtq_decode_attn_noalloc(ctypes.byref(cfg.c()), _ptr(layout.blob), layer, _ptr(q),
+                                              _ptr(ctx_len), max_ctx, ctypes.byref(cache.c()), _ptr(out), n_splits,
+                                              _stream(stream)))
     return out
 
 

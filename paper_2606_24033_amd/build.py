@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libblockgtq.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["blockgtq.cpp", "kernels.hip", "decode_f16.hip", "prefill.hip", "window.hip", "step.hip", "probe.hip", "quantize.hip"] + [f"decode_bv{b}.hip" for b in range(1, 9)]
+SOURCES = ["blockgtq.cpp", "kernels.hip", "decode_f16.hip", "prefill.hip", "window.hip", "step.hip", "probe.hip", "quantize.hip", "noalloc.hip"] + [f"decode_bv{b}.hip" for b in range(1, 9)]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

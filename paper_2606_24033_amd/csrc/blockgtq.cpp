@@ -587,6 +587,37 @@ int blockgtq_decode_attn(const bgtq_config* cfg, const void* d_layout, int32_t l
   return ok();
 }
 
+int blockgtq_decode_attn_noalloc(const bgtq_config* cfg, const void* d_layout, int32_t layer, const void* d_q,
+                                 const int32_t* d_ctx_len, int32_t max_ctx, const bgtq_cache* cache, float* d_out,
+                                 int32_t n_splits, void* stream) {
+  if (int e = check_cfg(cfg)) return e;
+  if (layer < -1 || layer >= cfg->n_layers) return fail(BGTQ_EINVAL, "layer %d out of range", layer);
+  if (max_ctx < 0 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [0, capacity]", max_ctx);
+  if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);
+  const int n_lc = layer < 0 ? cfg->n_layers : 1;
+  const size_t need = ws_bytes_of(cfg, n_lc, plan_splits(cfg, n_lc, max_ctx, n_splits));
+  if (need > BGTQ_NOALLOC_SCRATCH_BYTES)
+    return fail(BGTQ_EWORKSPACE, "this call needs %zu bytes of workspace, more than the %u-byte static array",
+                need, BGTQ_NOALLOC_SCRATCH_BYTES);
+  void* ws_ptr = nullptr;
+  hipError_t e = noalloc_scratch(&ws_ptr);
+  if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+  DecodeWs ws;
+  if (int rc = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, ws_ptr, BGTQ_NOALLOC_SCRATCH_BYTES,
+                                 n_splits, &ws))
+    return rc;
+  if (!d_layout || !cache || !cache->k_codes || !cache->k_norms || !cache->v_codes || !cache->v_norms)
+    return fail(BGTQ_EINVAL, "NULL pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  e = launch_clear_counters(ws.counters, n_lc * cfg->batch * cfg->n_kv_heads, s);
+  if (e != hipSuccess) return hip_fail(e, "clear_counters launch");
+  CachePtrs c{static_cast<uint32_t*>(cache->k_codes), static_cast<uint16_t*>(cache->k_norms),
+              static_cast<uint32_t*>(cache->v_codes), static_cast<uint16_t*>(cache->v_norms)};
+  e = launch_decode_packed(dims_of(cfg, layer), d_layout, d_q, d_ctx_len, c, d_out, ws, s);
+  if (e != hipSuccess) return hip_fail(e, "decode_attn_noalloc launch");
+  return ok();
+}
+
 int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void* d_q, const int32_t* d_ctx_len,
                               int32_t max_ctx, const void* d_k16, const void* d_v16, float* d_out,
                               void* d_workspace, size_t ws_bytes, int32_t n_splits, void* stream) {

@@ -102,4 +102,10 @@ hipError_t launch_prefill_attn(const Dims& d, const void* layout, const void* q,
 // writes sink[0] only in a case no real input reaches (probe.hip).
 hipError_t launch_read_probe(const void* src, size_t bytes, uint32_t* sink, hipStream_t s);
 
+// No-allocation decode (noalloc.hip): the current device's static scratch
+// array (BGTQ_NOALLOC_SCRATCH_BYTES), its address looked up once per device;
+// and a fill kernel that zeroes n split counters.
+hipError_t noalloc_scratch(void** out);
+hipError_t launch_clear_counters(int32_t* counters, int n, hipStream_t s);
+
 }  // namespace bgtq
