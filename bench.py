@@ -78,6 +78,9 @@ def parse():
                     help="skip the other workloads (toy, Qwen-shaped 32K layer / 128K / 256K / 512K, ragged batch)")
     ap.add_argument("--no-long", action="store_true", help="skip the 256K and 512K Qwen-shaped steps")
     ap.add_argument("--only-headline", action="store_true", help="the headline step and its roofline only")
+    ap.add_argument("--model", choices=["llama8b_k2v2", "qwen3b_k3v3"], default="llama8b_k2v2",
+                    help="workload of the headline step (qwen3b_k3v3: 36 layers x 2 KV heads, G = 8, K3V3, "
+                         "8192-row prefill chunks; for profiles with --only-headline)")
     ap.add_argument("--cpu-workers", type=int, default=0, help="CPU baseline processes (0: host CPUs, at most 16)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one plain device copy of this size first (HBM counter calibration)")
@@ -677,7 +680,7 @@ def _cpu_model():
     return "unknown"
 
 
-def cpu_oracle_baseline(bits, T, workers, budget_s=8.0):
+def cpu_oracle_baseline(bits, T, workers, spec=LLAMA, budget_s=8.0):
     """The fp64 CPU oracle (rotated form, as it stands) on a bounded sample of
     the headline step: `workers` processes, one host core and one (layer, KV
     head) unit each; after every cache is built, all run decode steps of their
@@ -686,11 +689,11 @@ def cpu_oracle_baseline(bits, T, workers, budget_s=8.0):
     process in the same phase."""
     import multiprocessing as mp
     ctx = mp.get_context("spawn")
-    L, H = LLAMA["n_layers"], LLAMA["n_kv"]
+    L, H = spec["n_layers"], spec["n_kv"]
     units = [divmod((w * 37) % (L * H), H) for w in range(workers)]   # spread over layers and heads
     barrier = ctx.Barrier(workers)
     queue = ctx.Queue()
-    procs = [ctx.Process(target=_cpu_unit_worker, args=(w, units[w], LLAMA, T, bits, budget_s, barrier, queue))
+    procs = [ctx.Process(target=_cpu_unit_worker, args=(w, units[w], spec, T, bits, budget_s, barrier, queue))
              for w in range(workers)]
     t_start = time.time()
     for p in procs:
@@ -707,7 +710,7 @@ def cpu_oracle_baseline(bits, T, workers, budget_s=8.0):
     return {"value": round(nbytes / (t1 - t0) / 1e9, 4), "unit": "GB/s", "cores": int(workers), "kind": "oracle",
             "sample": f"{workers} (layer, KV head) units of the headline step, one process (one thread) each, "
                       f"{steps} decode steps in all at ctx {T + 1}.. (encode the appended row + rotated-form fp64 "
-                      f"attention of 4 query heads), {t1 - t0:.2f} s wall for the timed phase; caches built "
+                      f"attention of {spec['group']} query heads), {t1 - t0:.2f} s wall for the timed phase; caches built "
                       f"untimed ({t0 - t_start:.1f} s)",
             "one_thread_gbs": round(one / 1e9, 4), "one_thread_s_per_unit_step": round(per_step_unit_s, 3),
             "cpu_model": _cpu_model(), "host_cpus": len(os.sched_getaffinity(0)),
@@ -735,7 +738,9 @@ def main():
     want_fp16 = not args.no_fp16 and not args.only_headline
     want_win = not args.no_protected and not args.only_headline
     t_setup = time.time()
-    m = Model(bg, synth, torch, LLAMA, T, W + K, fp16=want_fp16, window=want_win, n_splits=args.n_splits)
+    spec = LLAMA if args.model == "llama8b_k2v2" else QWEN_LONG
+    m = Model(bg, synth, torch, spec, T, W + K, fp16=want_fp16, window=want_win, n_splits=args.n_splits,
+              chunk=None if spec is LLAMA else 8192)
     log(f"setup {time.time() - t_setup:.1f} s (prefill of {T} rows x {m.L} layers x {m.H} heads)")
     if args.copy_calib_mib > 0:
         # a plain copy of known size: FETCH_SIZE / WRITE_SIZE of this dispatch
@@ -770,8 +775,10 @@ def main():
         "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": W,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f16", "data": "synthetic",
-        "config": {"workload": "Llama-3.1-8B-shaped full decode step: 32 layers x 8 KV heads (32 q heads), "
-                               f"d_h 128, {T} cached rows, K2V2, batch 1, bf16 inputs",
+        "config": {"workload": ("Llama-3.1-8B-shaped full decode step: 32 layers x 8 KV heads (32 q heads), "
+                                f"d_h 128, {T} cached rows, K2V2, batch 1, bf16 inputs") if spec is LLAMA else
+                               ("Qwen2.5-3B-shaped full decode step: 36 layers x 2 KV heads (16 q heads), "
+                                f"d_h 128, {T} cached rows, K3V3, batch 1, bf16 inputs"),
                    "global_batch": 1, "seq_len": T, "parallelism": "none (1 GPU)", "n_splits": args.n_splits},
         "settle": settled,
         "us_per_step": round(ms_per_step * 1e3, 2),
@@ -789,7 +796,7 @@ def main():
                           "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
                           "traffic": None if traffic is None else int(traffic),
                           "kernel": "k_split_mfma (one launch per decode call: query rotation, split pass, "
-                                    "merge), all 32 layers",
+                                    f"merge), all {m.L} layers",
                           "algorithmic_bytes_per_launch": int(step_bytes),
                           "launch_us_mean": round(dec_mean, 2),
                           "launch_us_median": round(float(np.median(dec_us)), 2)}
@@ -870,7 +877,7 @@ def main():
 
     if not args.no_cpu and not args.only_headline:
         workers = args.cpu_workers or min(16, len(os.sched_getaffinity(0)))
-        result["cpu_baseline"] = cpu_oracle_baseline(bits_llama, T, workers)
+        result["cpu_baseline"] = cpu_oracle_baseline(bits_llama, T, workers, spec)
     print(json.dumps(result), flush=True)
 
 

@@ -206,10 +206,13 @@ struct SplitPlan {
   int n_splits, split_len;
 };
 
-// Default split count: the decode kernels run one 16-wave workgroup per CU at
-// a time, two rounds (the second round's workgroups go to the CUs that finish
-// first, so the work evens out), each split at least 1024 rows (a 64-row tile
-// per wave).
+// Default split count.  The decode kernels run one 16-wave workgroup per CU
+// (256 CUs), so a launch of U units x n splits takes ceil(U n / 256) rounds,
+// each as long as one split: ceil(split length / 1024) 64-row tile
+// iterations per wave plus ~2 iterations of set-up and merge.  The plan
+// minimises rounds x split time over n; a single round pays 1.15x for the
+// spread of per-row costs (the most expensive row decides it), which a second
+// round fills in.  Each split covers at least one tile per wave.
 SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested) {
   SplitPlan p;
   if (max_ctx <= 0) return {1, 64};
@@ -219,8 +222,19 @@ SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested
     n = std::min(requested, max_splits);
   } else {
     const long units = static_cast<long>(c->n_kv_heads) * c->batch * n_lc;
-    n = static_cast<int>((512 + units - 1) / units);
-    n = std::max(1, std::min(n, (max_ctx + 1023) / 1024));
+    const int n_hi = std::max(1, std::min(64, (max_ctx + 1023) / 1024));
+    double best = 0.0;
+    n = 1;
+    for (int k = 1; k <= n_hi; ++k) {
+      const int len = ((max_ctx + k - 1) / k + 63) / 64 * 64;
+      const long rounds = (units * k + 255) / 256;
+      double t = static_cast<double>(rounds) * ((len + 1023) / 1024 + 2);
+      if (rounds == 1) t *= 1.15;
+      if (k == 1 || t < best) {
+        best = t;
+        n = k;
+      }
+    }
   }
   p.split_len = ((max_ctx + n - 1) / n + 63) / 64 * 64;
   p.n_splits = (max_ctx + p.split_len - 1) / p.split_len;

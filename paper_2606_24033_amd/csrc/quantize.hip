@@ -9,18 +9,18 @@
 // (k-step s of lane l pairs with dim 32 (l / 16) + s): a lane loads its slice
 // of a row with 16-byte loads and no gather.
 //
-//  k_quant_keys   : Z = W X^T.  W (the layout's dense key rotation on the
-//                   natural dims, the gather into stream order folded in) is
-//                   the A operand, staged in LDS once per workgroup; the key
-//                   rows are the B operand.  A lane ends with four
-//                   consecutive stream positions of one row, i.e. one
-//                   contiguous bit field of the packed row.  The group radii
-//                   come from the same kind of product, a 0/1 group
-//                   membership matrix times the squared inputs.
-//  k_quant_values : Z = X Pi_V^T.  The value rows are the A operand, Pi_V the
-//                   B operand.  A lane ends with one coordinate of four
-//                   consecutive rows, i.e. one contiguous bit field of a
-//                   32-row value tile.
+// One launch (k_quant_rows) for both: its first workgroups encode keys, the
+// others values.
+//  keys   : Z = W X^T.  W (the layout's dense key rotation on the natural
+//           dims, the gather into stream order folded in) is the A operand,
+//           staged in LDS once per workgroup; the key rows are the B
+//           operand.  A lane ends with four consecutive stream positions of
+//           one row, i.e. one contiguous bit field of the packed row.  The
+//           group radii come from the same kind of product, a 0/1 group
+//           membership matrix times the squared inputs.
+//  values : Z = X Pi_V^T.  The value rows are the A operand, Pi_V the B
+//           operand.  A lane ends with one coordinate of four consecutive
+//           rows, i.e. one contiguous bit field of a 32-row value tile.
 // Codes: number of thresholds <= z (binary search over the fp32 midpoints of
 // the fp16 centroids, LDS); rows and tiles are assembled in LDS with atomic
 // ORs and written with whole-word stores.
@@ -38,10 +38,6 @@ typedef float float4_t __attribute__((ext_vector_type(4)));
 constexpr int kWaves = 16;
 constexpr int kThreads = kWaves * 64;
 constexpr int kSub = 16;                          // rows per wave sub-tile (one MFMA column block)
-constexpr int kKIters = 2;                        // key sub-tiles per wave
-constexpr int kKRows = kWaves * kSub * kKIters;   // rows per key workgroup
-constexpr int kVIters = 2;                        // value tiles per wave
-constexpr int kVTiles = kWaves * kVIters;         // 32-row value tiles per value workgroup
 constexpr int kMatF4 = kMfmaMatFloats / 4;        // float4 entries of one MFMA-order matrix
 
 struct LdsK {
@@ -116,12 +112,12 @@ __device__ __forceinline__ float4_t mfma(float a, float b, float4_t c) {
 }
 
 // ---------------------------------------------------------------- keys
-// grid (ceil(rows / kKRows), n_kv, batch x layers in the call)
+// Workgroup bx of the key part: rows [bx R, bx R + R) of the call, R =
+// kWaves kSub iters.
 template <bool BF16>
-__global__ __launch_bounds__(kThreads) void k_quant_keys(Dims d, const uint8_t* __restrict__ blob,
-                                                         const void* __restrict__ kin, int n_new,
-                                                         const int32_t* __restrict__ wpos, CachePtrs c) {
-  __shared__ __attribute__((aligned(16))) LdsK S;
+__device__ __forceinline__ void quant_keys(LdsK& S, int bx, int iters, const Dims& d,
+                                           const uint8_t* __restrict__ blob, const void* __restrict__ kin, int n_new,
+                                           const int32_t* __restrict__ wpos, const CachePtrs& c) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, lz = blockIdx.z;
   const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
@@ -130,7 +126,7 @@ __global__ __launch_bounds__(kThreads) void k_quant_keys(Dims d, const uint8_t* 
   const int wp = wpos[seq];
   if (wp < 0 || wp >= cap) return;
   const int n_fit = min(n_new, cap - wp);  // rows that fit (the host rejects overflow)
-  const int r_wg = blockIdx.x * kKRows;
+  const int r_wg = bx * kWaves * kSub * iters;
   if (r_wg >= n_fit) return;
   const int n_rows_blob = d.n_layers * d.n_kv;
   const int ri = layer * d.n_kv + head;
@@ -161,7 +157,7 @@ __global__ __launch_bounds__(kThreads) void k_quant_keys(Dims d, const uint8_t* 
   const int tk = lane & 15, kk = lane >> 4;
   const int kw = d.k_words, nslot = (ng + 1) & ~1;
   const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + head;
-  for (int it = 0; it < kKIters; ++it) {
+  for (int it = 0; it < iters; ++it) {
     const int r0 = r_wg + (it * kWaves + wave) * kSub;
     if (r0 >= n_fit) break;  // wave-uniform
     const int r = r0 + tk;
@@ -238,14 +234,14 @@ __global__ __launch_bounds__(kThreads) void k_quant_keys(Dims d, const uint8_t* 
 }
 
 // ---------------------------------------------------------------- values
-// grid (ceil(tiles / kVTiles), n_kv, batch x layers in the call).  A wave
-// owns whole 32-row value tiles; the words of a tile partly outside
-// [write_pos, write_pos + n_new) keep the bits of the other rows.
+// Workgroup bx of the value part: value tiles [bx T, bx T + T) of the rows
+// the call touches, T = kWaves iters.  A wave owns whole 32-row value tiles;
+// the words of a tile partly outside [write_pos, write_pos + n_new) keep the
+// bits of the other rows.
 template <bool BF16>
-__global__ __launch_bounds__(kThreads) void k_quant_values(Dims d, const uint8_t* __restrict__ blob,
-                                                           const void* __restrict__ vin, int n_new,
-                                                           const int32_t* __restrict__ wpos, CachePtrs c) {
-  __shared__ __attribute__((aligned(16))) LdsV S;
+__device__ __forceinline__ void quant_values(LdsV& S, int bx, int iters, const Dims& d,
+                                             const uint8_t* __restrict__ blob, const void* __restrict__ vin,
+                                             int n_new, const int32_t* __restrict__ wpos, const CachePtrs& c) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int head = blockIdx.y, lz = blockIdx.z;
   const int layer = d.layer >= 0 ? d.layer : lz / d.batch;
@@ -255,7 +251,7 @@ __global__ __launch_bounds__(kThreads) void k_quant_values(Dims d, const uint8_t
   if (wp < 0 || wp >= cap) return;
   const int n_fit = min(n_new, cap - wp);
   const int tile0 = wp / kTile, n_tiles = (wp + n_fit - 1) / kTile - tile0 + 1;
-  const int tw0 = blockIdx.x * kVTiles;
+  const int tw0 = bx * kWaves * iters;
   if (tw0 >= n_tiles) return;
   const int n_rows_blob = d.n_layers * d.n_kv;
   const float4* rsrc = reinterpret_cast<const float4*>(blob + layout_rotv_mfma_offset(n_rows_blob));
@@ -268,7 +264,7 @@ __global__ __launch_bounds__(kThreads) void k_quant_values(Dims d, const uint8_t
   const float* thr = S.thr + thr_index(bv);
   const float sq = sqrtf(static_cast<float>(kHeadDim));
   const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + head;
-  for (int it = 0; it < kVIters; ++it) {
+  for (int it = 0; it < iters; ++it) {
     const int tw = tw0 + it * kWaves + wave;
     if (tw >= n_tiles) break;  // wave-uniform
     const int tile = tile0 + tw, P0 = tile * kTile;
@@ -348,6 +344,22 @@ __global__ __launch_bounds__(kThreads) void k_quant_values(Dims d, const uint8_t
   }
 }
 
+// One launch for both parts: workgroups [0, n_kwg) encode keys, the rest
+// values; grid (n_kwg + n_vwg, n_kv, batch x layers in the call).
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void k_quant_rows(Dims d, const uint8_t* __restrict__ blob,
+                                                         const void* __restrict__ kin, const void* __restrict__ vin,
+                                                         int n_new, const int32_t* __restrict__ wpos, CachePtrs c,
+                                                         int n_kwg, int k_iters, int v_iters) {
+  constexpr size_t kBytes = sizeof(LdsK) > sizeof(LdsV) ? sizeof(LdsK) : sizeof(LdsV);
+  __shared__ __attribute__((aligned(16))) uint8_t smem[kBytes];
+  const int bx = static_cast<int>(blockIdx.x);
+  if (bx < n_kwg)
+    quant_keys<BF16>(*reinterpret_cast<LdsK*>(smem), bx, k_iters, d, blob, kin, n_new, wpos, c);
+  else
+    quant_values<BF16>(*reinterpret_cast<LdsV*>(smem), bx - n_kwg, v_iters, d, blob, vin, n_new, wpos, c);
+}
+
 }  // namespace quant_detail
 
 hipError_t launch_quantize_prefill(const Dims& d, const void* layout, const void* k, const void* v, int n_new,
@@ -355,15 +367,21 @@ hipError_t launch_quantize_prefill(const Dims& d, const void* layout, const void
   using namespace quant_detail;
   const uint8_t* blob = static_cast<const uint8_t*>(layout);
   const int lz = d.batch * d.n_lc;
-  const dim3 gk((n_new + kKRows - 1) / kKRows, d.n_kv, lz);
-  const dim3 gv((n_new / kTile + 2 + kVTiles - 1) / kVTiles, d.n_kv, lz);
-  if (d.in_dtype == 1) {
-    hipLaunchKernelGGL(k_quant_keys<true>, gk, dim3(kThreads), 0, s, d, blob, k, n_new, write_pos, c);
-    hipLaunchKernelGGL(k_quant_values<true>, gv, dim3(kThreads), 0, s, d, blob, v, n_new, write_pos, c);
-  } else {
-    hipLaunchKernelGGL(k_quant_keys<false>, gk, dim3(kThreads), 0, s, d, blob, k, n_new, write_pos, c);
-    hipLaunchKernelGGL(k_quant_values<false>, gv, dim3(kThreads), 0, s, d, blob, v, n_new, write_pos, c);
-  }
+  // rows per workgroup: small calls spread over more workgroups (one
+  // sub-tile or value tile per wave), large ones amortise the 64 KB matrix
+  // staged in LDS over more rows
+  const long rows = static_cast<long>(n_new) * d.n_kv * lz;
+  const int k_iters = rows <= 256L * 256 ? 1 : (rows <= 4L * 256 * 512 ? 2 : 4);
+  const int v_iters = rows <= 256L * 512 ? 1 : 2;
+  const int n_kwg = (n_new + kWaves * kSub * k_iters - 1) / (kWaves * kSub * k_iters);
+  const int n_vwg = (n_new / kTile + 2 + kWaves * v_iters - 1) / (kWaves * v_iters);
+  const dim3 grid(n_kwg + n_vwg, d.n_kv, lz);
+  if (d.in_dtype == 1)
+    hipLaunchKernelGGL(k_quant_rows<true>, grid, dim3(kThreads), 0, s, d, blob, k, v, n_new, write_pos, c, n_kwg,
+                       k_iters, v_iters);
+  else
+    hipLaunchKernelGGL(k_quant_rows<false>, grid, dim3(kThreads), 0, s, d, blob, k, v, n_new, write_pos, c, n_kwg,
+                       k_iters, v_iters);
   return hipGetLastError();
 }
 
