@@ -56,6 +56,12 @@ typedef float float4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 16;  // one workgroup per CU: 160 KB of LDS for the tables
 constexpr int kThreads = kWaves * 64;
+// Waves of a packed-decode workgroup: 16 (4 per SIMD) with one query set;
+// 12 with two (3 per SIMD, up to 168 VGPRs for the doubled accumulators:
+// -10 to -13 % decode time against 16 waves that spill, measured at 128K and
+// 512K rows).
+template <int NSET>
+constexpr int split_waves() { return NSET == 1 ? 16 : 12; }
 constexpr int kMaxSlots = 10;  // 16-step query slots of one key row: sum_g ceil(steps_g / 16)
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLog2e = 1.4426950408889634f;
@@ -564,7 +570,7 @@ __device__ __forceinline__ float merge_window(const float* __restrict__ w, float
   return e;
 }
 
-template <int NSET>
+template <int NSET, int WAVES>
 __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims& d, int G, int lz, int kvh,
                                             int split, int tid, int lane, int wave, float (&m_run)[NSET],
                                             float (&l_run)[NSET], const float4_t (&O)[NSET][2],
@@ -579,8 +585,8 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
   // ---------------- merge the waves of the workgroup
   __syncthreads();
   float* fm = reinterpret_cast<float*>(smem);            // [wave][8] max
-  float* fl = fm + kWaves * 8;                           // [wave][8] sum
-  float* fo = fl + kWaves * 8;                           // [wave][8][128] accumulators
+  float* fl = fm + WAVES * 8;                           // [wave][8] sum
+  float* fo = fl + WAVES * 8;                           // [wave][8][128] accumulators
 #pragma unroll
   for (int s = 0; s < NSET; ++s) {
     if (bq == 0) {
@@ -593,15 +599,15 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
       for (int r = 0; r < 4; ++r) fo[(wave * 8 + s * 4 + r) * kHeadDim + 64 * h + lane] = O[s][h][r];
   }
   __syncthreads();
-  float* os = fo + kWaves * 8 * kHeadDim;  // [G][128] merged output, rotated V domain
+  float* os = fo + WAVES * 8 * kHeadDim;  // [G][128] merged output, rotated V domain
   float* ws_ = os + 8 * kHeadDim;          // [G][128] weight of the window's accumulator
-  for (int i = tid; i < G * kHeadDim; i += kThreads) {
+  for (int i = tid; i < G * kHeadDim; i += (WAVES * 64)) {
     const int qh = i >> 7, dd = i & 127;
     float mx = kNegInf;
-    for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, fm[w * 8 + qh]);
+    for (int w = 0; w < WAVES; ++w) mx = fmaxf(mx, fm[w * 8 + qh]);
     float l = 0.f, a = 0.f;
     if (mx != kNegInf) {
-      for (int w = 0; w < kWaves; ++w) {
+      for (int w = 0; w < WAVES; ++w) {
         const float mw = fm[w * 8 + qh];
         if (mw == kNegInf) continue;
         const float e = exp2_hw(mw - mx);
@@ -652,7 +658,7 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
               n_splits - 1;
     __syncthreads();
     if (*last == 0) return;
-    for (int i = tid; i < G * kHeadDim; i += kThreads) {
+    for (int i = tid; i < G * kHeadDim; i += (WAVES * 64)) {
       const int qh = i >> 7, dd = i & 127;
       const float* P = part + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits * 130;
       const auto ld = [](const float* x) { return __hip_atomic_load(x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
@@ -697,7 +703,7 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
   }
   __syncthreads();
   // ---------------- out = Pi_V^T o (back from the rotated V domain), or o
-  for (int i = tid; i < G * kHeadDim; i += kThreads) {
+  for (int i = tid; i < G * kHeadDim; i += (WAVES * 64)) {
     const int qh = i >> 7, dd = i & 127;
     float r = os[i];
     if (rotv != nullptr) {
@@ -711,10 +717,13 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
 
 // ---------------------------------------------------------------- kernel
 template <int NSET, int KWB, int BV>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 16 ? 3 : 4))) void k_split_mfma(
+__global__ __launch_bounds__(split_waves<NSET>() * 64)
+__attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_split_mfma(
     Dims d, const uint8_t* __restrict__ blob, const void* __restrict__ q, const int32_t* __restrict__ ctx_len,
     CachePtrs c, float* __restrict__ out, int32_t* __restrict__ counters, float* __restrict__ part, int n_splits,
     int split_len, WinArgs win) {
+  // this instantiation's workgroup (shadows the comparator's 16 waves)
+  constexpr int kWaves = split_waves<NSET>(), kThreads = kWaves * 64;
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: tile addresses stay scalar
@@ -754,7 +763,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
   // rotated (qr).
   static_assert((2 * 8 * kHeadDim + kRowRotFloats + 8 * kHeadDim) * 4 + kHeadDim <= kQimg,
                 "set-up staging must stay below the query image");
-  static_assert(8 * kHeadDim <= kThreads, "one query coordinate per thread");
   float* qg = reinterpret_cast<float*>(smem);      // [G][128] queries in stream order
   float* qr = qg + 8 * kHeadDim;                   // [G][128] rotated
   float* rs = qr + 8 * kHeadDim;                   // the row's rotations, <= 128^2 floats
@@ -790,6 +798,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     for (int u = 0; u < kRotFirst; ++u) rv[u] = rowrot[tid + u * kThreads];
     if (tid < G * kHeadDim) qn[tid] = __uint_as_float(bf ? ((qi & 1) ? qw & 0xFFFF0000u : qw << 16) : qw);
     if (tid < 32) dimw[tid] = mw;
+    // (fewer threads than query coordinates: the rest in a second round)
+    for (int i = tid + kThreads; i < G * kHeadDim; i += kThreads)
+      qn[i] = ld_q(q, (static_cast<size_t>(lz) * hqn + kvh * G) * kHeadDim + i, d.in_dtype);
     if (tid < kCodebookEntries) cbs[tid] = static_cast<uint16_t>(cv);
 #pragma unroll
     for (int u = 0; u < kRotFirst; ++u)
@@ -798,12 +809,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     for (int i = tid + kRotFirst * kThreads; i < rtot; i += kThreads) rs[i] = rowrot[i];
   }
   __syncthreads();
-  if (tid < G * kHeadDim)
-    qg[tid] = qn[(tid >> 7) * kHeadDim + reinterpret_cast<const uint8_t*>(dimw)[tid & 127]];
+  for (int e = tid; e < G * kHeadDim; e += kThreads)
+    qg[e] = qn[(e >> 7) * kHeadDim + reinterpret_cast<const uint8_t*>(dimw)[e & 127]];
   __syncthreads();
-  if (tid < G * kHeadDim) {
-    // one rotated coordinate per thread: p = stream position, g its group
-    const int h = tid >> 7, p = tid & 127;
+  for (int e = tid; e < G * kHeadDim; e += kThreads) {
+    // one rotated coordinate per thread and round: p = stream position, g its group
+    const int h = e >> 7, p = e & 127;
     int dg = rdim[0], off = roff[0], p0 = rpos[0];
 #pragma unroll
     for (int g = 1; g < kMaxGroups; ++g)
@@ -828,7 +839,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
       a1 = fmaf(rt[(k + 1) * dg + j], qq[k + 1], a1);
     }
     // log2(e) folded in: logits come out in base-2 units for exp2
-    qr[tid] = ((a0 + a1) + (a2 + a3)) * (kLog2e / sqrtf(static_cast<float>(dg) * kHeadDim));
+    qr[e] = ((a0 + a1) + (a2 + a3)) * (kLog2e / sqrtf(static_cast<float>(dg) * kHeadDim));
   }
   __syncthreads();
   // ---- query image: slot s, lane 4b+i holds step 16(s - slot0_g) + b of
@@ -1065,9 +1076,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KWB > 
     __builtin_amdgcn_s_setprio(0);
   }
 
-  finish_unit<NSET>(smem, reinterpret_cast<int*>(smem + kGmeta), d, G, lz, kvh, split, tid, lane, wave, m_run, l_run,
-                    O, counters, part, n_splits, 0.08838834764831845f /* 1/sqrt(d_h) */,
-                    reinterpret_cast<const float*>(blob + kOffRotV), out, win.part);
+  finish_unit<NSET, kWaves>(smem, reinterpret_cast<int*>(smem + kGmeta), d, G, lz, kvh, split, tid, lane, wave,
+                            m_run, l_run, O, counters, part, n_splits, 0.08838834764831845f /* 1/sqrt(d_h) */,
+                            reinterpret_cast<const float*>(blob + kOffRotV), out, win.part);
 }
 
 // ---------------------------------------------------------------- fp16 comparator
@@ -1276,8 +1287,8 @@ __global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __res
     __builtin_amdgcn_s_setprio(0);
   }
   __syncthreads();
-  finish_unit<NSET>(smem, reinterpret_cast<int*>(smem + kF16Flag), d, G, lz, kvh, split, tid, lane, wave, m_run, l_run,
-                    O, counters, part, n_splits, 1.f, nullptr, out, nullptr);
+  finish_unit<NSET, kWaves>(smem, reinterpret_cast<int*>(smem + kF16Flag), d, G, lz, kvh, split, tid, lane, wave,
+                            m_run, l_run, O, counters, part, n_splits, 1.f, nullptr, out, nullptr);
 }
 
 inline hipError_t launch_f16_mfma_impl(const Dims& d, const void* q, const int32_t* ctx_len, const void* k16,
@@ -1298,18 +1309,19 @@ hipError_t launch_split_bv_impl(const Dims& d, const void* layout, const void* q
                                 const CachePtrs& c, float* out, const DecodeWs& ws, hipStream_t s) {
   dim3 grid(ws.n_splits * d.n_kv * d.batch * d.n_lc);
   const uint8_t* blob = static_cast<const uint8_t*>(layout);
-  const auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, d, blob, q, ctx_len, c, out, ws.counters, ws.part,
+  const auto go = [&](auto kern, int threads) {
+    hipLaunchKernelGGL(kern, grid, dim3(threads), 0, s, d, blob, q, ctx_len, c, out, ws.counters, ws.part,
                        ws.n_splits, ws.split_len, WinArgs{ws.wpart, ws.n_sink, ws.n_recent});
   };
+  constexpr int t1 = split_waves<1>() * 64, t2 = split_waves<2>() * 64;
   if (d.group <= 4) {
-    if (d.k_words <= 8) go(k_split_mfma<1, 8, BV>);
-    else if (d.k_words <= 16) go(k_split_mfma<1, 16, BV>);
-    else go(k_split_mfma<1, 32, BV>);
+    if (d.k_words <= 8) go(k_split_mfma<1, 8, BV>, t1);
+    else if (d.k_words <= 16) go(k_split_mfma<1, 16, BV>, t1);
+    else go(k_split_mfma<1, 32, BV>, t1);
   } else {
-    if (d.k_words <= 8) go(k_split_mfma<2, 8, BV>);
-    else if (d.k_words <= 16) go(k_split_mfma<2, 16, BV>);
-    else go(k_split_mfma<2, 32, BV>);
+    if (d.k_words <= 8) go(k_split_mfma<2, 8, BV>, t2);
+    else if (d.k_words <= 16) go(k_split_mfma<2, 16, BV>, t2);
+    else go(k_split_mfma<2, 32, BV>, t2);
   }
   return hipGetLastError();
 }
