@@ -506,7 +506,7 @@ def quantize_roofline(m, label):
             "call_us": stats(us), "rows_per_s": round(rows_per_call * m.H / (mean_us * 1e-6), 1),
             "flops_per_row": round(fl_head / m.H, 1),
             "roofline": {"bound": "mfma", "achieved": round(tfl, 2), "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                         "frac": round(tfl / FP32_PEAK_TFLOPS, 4), "kernel": "k_quantize"}}
+                         "frac": round(tfl / FP32_PEAK_TFLOPS, 4), "kernel": "k_quant_rows"}}
 
 
 def ragged_workload(bg, synth, torch, args, flush_bytes=1 << 30):
@@ -605,7 +605,7 @@ def ragged_workload(bg, synth, torch, args, flush_bytes=1 << 30):
                                 "roofline": {"bound": "mfma", "achieved": round(B * chunk * fl / (pm * 1e-6) / 1e12, 2),
                                              "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
                                              "frac": round(B * chunk * fl / (pm * 1e-6) / 1e12 / FP32_PEAK_TFLOPS, 4),
-                                             "kernel": "k_quantize"}}}
+                                             "kernel": "k_quant_rows"}}}
     del cache, layout, flush, knew, vnew, q, out, ws, kv
     torch.cuda.empty_cache()
     return res
