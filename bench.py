@@ -298,6 +298,29 @@ def timed_steps(torch, m, first, n):
             g0.elapsed_time(g1))
 
 
+def sdpa_decode_context(torch, m, W, K):
+    """Context for the fp16 comparator: torch's scaled_dot_product_attention
+    (fp16, one query row per head, grouped KV heads) over the same fp16 cache,
+    all layers in one call (layers as the batch).  None if torch refuses."""
+    try:
+        sdpa = torch.nn.functional.scaled_dot_product_attention
+        ctx = int(m.ctxs[W].item())
+        k = m.k16[:, 0, :, :ctx]
+        v = m.v16[:, 0, :, :ctx]
+        qs = [m.q[W + i][:, 0].half()[:, :, None] for i in range(min(K, 8))]
+        fn = lambda i: sdpa(qs[i % len(qs)], k, v, enable_gqa=True)
+        fn(0)
+        torch.cuda.synchronize()
+        us = interleaved(torch, [fn], K)[0]
+        byt = m.fp16_bytes(ctx) + m.io_bytes()
+        return {"call_us": stats(us), "gbs": round(byt / (np.median(us) * 1e-6) / 1e9, 2),
+                "pct_hbm_peak": round(100 * byt / (np.median(us) * 1e-6) / 1e9 / HBM_PEAK_GBS, 2),
+                "note": "torch fp16 SDPA, q_len 1, enable_gqa, layers as the batch; context only"}
+    except Exception as e:  # noqa: BLE001 - context only
+        log(f"torch SDPA decode context unavailable: {e}")
+        return None
+
+
 def workload_line(torch, m, args, label, settle_s, fp16=False):
     """Settle, K timed steps, then (fp16) the packed and fp16 decodes
     interleaved at the timed steps' contexts."""
@@ -330,6 +353,9 @@ def workload_line(torch, m, args, label, settle_s, fp16=False):
             "gbs": round(fb / (np.mean(f_us) * 1e-6) / 1e9, 2),
             "pct_hbm_peak": round(100 * fb / (np.mean(f_us) * 1e-6) / 1e9 / HBM_PEAK_GBS, 2),
             "speedup_packed_over_fp16": round(float(np.median(f_us) / np.median(p_us)), 3)}
+        sd = sdpa_decode_context(torch, m, W, args.steps)
+        if sd is not None:
+            res["fp16_comparator"]["torch_sdpa_fp16_decode"] = sd
     return res
 
 
@@ -818,6 +844,9 @@ def main():
         result["fp16_decode_pct_hbm_peak"] = round(100 * fbytes / (np.mean(f_us) * 1e-6) / 1e9 / HBM_PEAK_GBS, 2)
         result["packed_decode_us_median_interleaved"] = round(float(np.median(p_us)), 2)
         result["speedup_vs_fp16_decode"] = round(float(np.median(f_us) / np.median(p_us)), 3)
+        sd = sdpa_decode_context(torch, m, W, K)
+        if sd is not None:
+            result["torch_sdpa_fp16_decode"] = sd
         del m.k16, m.v16
         torch.cuda.empty_cache()
 

@@ -622,7 +622,8 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
       if (wpart != nullptr) ws_[i] = l > 0.f ? e / l : 0.f;
     } else {
       // agent-scope stores: written through to the device coherence point
-      // (each XCD has its own L2), published by the release fence below
+      // (each XCD has its own L2), completed before the counter increment
+      // below
       float* pb = part + ((static_cast<size_t>(lz) * hqn + kvh * G + qh) * n_splits + split) * 130;
       __hip_atomic_store(pb + 2 + dd, a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (dd == 0) {
@@ -1083,17 +1084,27 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
 
 // ---------------------------------------------------------------- fp16 comparator
 // The same split-context decode over an uncompressed fp16 cache (keys and
-// values [rows][128]): the same work mapping, MFMA products, softmax and
-// merges, with no decode and no rotation.  Keys: lane = token reads its
-// 256-byte row in four 64-byte chunks (8 steps each), the next chunk in
-// flight.  Values: lane = dim gathers each 4-token step with 2-byte loads
-// (every load instruction reads one row's 128 contiguous bytes), half of a
-// tile issued with its keys and the other half after its QK products.
-constexpr int kF16Flag = (kWaves * 8 * 2 + kWaves * 8 * kHeadDim + 2 * 8 * kHeadDim) * 4;  // past the merge area
+// values [rows][128]): the same MFMA products, softmax and merges, with no
+// decode and no rotation.  It is bound by HBM reads, so its workgroups are 4
+// waves, one per SIMD: each wave has the SIMD's 512 registers (VGPRs and
+// AGPRs) and keeps the next 64-row tile in flight while it computes the
+// current one (about 300 registers; with two waves per SIMD, 256 each, the
+// same schedule spills):
+//  * keys: lane = token reads its 256-byte row with 16 loads of 16 bytes (two
+//    4-coordinate steps each), the B operand of QK as it arrives;
+//  * values: for each 4-token step and half of the dims, lane 4b + j reads 8
+//    bytes (dims 64 h + 4b .. +3 of token 4s + j); a 4x4 transpose of 16-bit
+//    elements inside each lane quad turns that into the PV B operand (4 tokens
+//    of dim 64 h + lane).  32 loads per tile instead of 128 two-byte gathers.
+// The next tile's keys are issued before the current QK products, its values
+// right after them (into the registers the keys leave).
+constexpr int kF16Waves = 4;
+constexpr int kF16Threads = kF16Waves * 64;
+constexpr int kF16Flag = (kF16Waves * 8 * 2 + kF16Waves * 8 * kHeadDim + 2 * 8 * kHeadDim) * 4;  // past the merge area
 constexpr int kF16Lds = kF16Flag + 16;
 
 template <int NSET, int S0, int... J>
-__device__ __forceinline__ void f16_qk_chunk(std::integer_sequence<int, J...>, const uint4 (&ka)[4],
+__device__ __forceinline__ void f16_qk_chunk(std::integer_sequence<int, J...>, const uint4* ka,
                                              const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
                                              float4_t (&L)[NSET]) {
   (qk_mac<NSET, (S0 + J) % 16>((J & 1) ? as_half4(ka[J >> 1].z, ka[J >> 1].w) : as_half4(ka[J >> 1].x, ka[J >> 1].y),
@@ -1101,45 +1112,177 @@ __device__ __forceinline__ void f16_qk_chunk(std::integer_sequence<int, J...>, c
    ...);
 }
 
-template <int NSET, int S0, int... S>
-__device__ __forceinline__ void f16_pv(std::integer_sequence<int, S...>, const half4_t (&vv)[8][2],
-                                       const half4_t (&pp)[NSET], float4_t (&O)[NSET][2]) {
-  (
-      [&] {
+// Keys of the tile at t0: lane = token, 16-byte chunks J0 .. J0 + 7 of its row.
+template <int J0>
+__device__ __forceinline__ void f16_load_keys(const _Float16* kb, int t0, int lane, uint4 (&k)[16]) {
+  const uint4* kr = reinterpret_cast<const uint4*>(kb + static_cast<size_t>(t0 + lane) * kHeadDim);
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+  for (int j = J0; j < J0 + 8; ++j) k[j] = kr[j];
+}
+// Values of steps S0 .. S0 + 7 of the tile at t0, untransposed: v[2 s + h] =
+// dims 64 h + 4 (lane / 4) .. +3 of token t0 + 4 s + lane % 4.
+template <int S0>
+__device__ __forceinline__ void f16_load_values(const _Float16* vb, int t0, int lane, uint2 (&v)[32]) {
+  const _Float16* base = vb + static_cast<size_t>(t0 + (lane & 3)) * kHeadDim + 4 * (lane >> 2);
 #pragma unroll
-          for (int s = 0; s < NSET; ++s)
-            O[s][h] = __builtin_amdgcn_mfma_f32_4x4x4f16(pp[s], vv[S][h], O[s][h], 4, S0 + S, 0);
-      }(),
-      ...);
+  for (int s = S0; s < S0 + 8; ++s)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      v[2 * s + h] = *reinterpret_cast<const uint2*>(base + static_cast<size_t>(4 * s) * kHeadDim + 64 * h);
 }
 
-// values of steps S0 .. S0 + 7 of the tile at t0: vv[s][h] = the 4 tokens of
-// step S0 + s at dim 64 h + lane
-template <int S0>
-__device__ __forceinline__ void f16_load_values(const _Float16* vb, int t0, int lane, half4_t (&vv)[8][2]) {
+// 4x4 transpose of 16-bit elements inside a lane quad: on entry lane j holds
+// row j (elements 0, 1 in .x, 2, 3 in .y); on exit column j (rows 0, 1 in .x,
+// 2, 3 in .y).  First 32-bit words move between lanes j and j ^ 2, then
+// 16-bit halves between j and j ^ 1 (byte selects per lane parity).
+struct QuadT16 {
+  bool hi2;
+  uint32_t sel_s, sel_0, sel_1;
+};
+__device__ __forceinline__ QuadT16 quad_t16_setup(int lane) {
+  const bool odd = lane & 1;
+  return QuadT16{(lane & 2) != 0, odd ? 0x05040100u : 0x07060302u, odd ? 0x03020504u : 0x05040100u,
+                 odd ? 0x03020706u : 0x07060100u};
+}
+__device__ __forceinline__ half4_t quad_t16(uint2 w, const QuadT16& t) {
+  const uint32_t x = t.hi2 ? w.x : w.y;
+  const uint32_t y = static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x4E, 0xF, 0xF, false));
+  const uint32_t a = t.hi2 ? y : w.x;  // rows j & 1,       columns 2 (j >> 1) .. +1
+  const uint32_t c = t.hi2 ? w.y : y;  // rows (j & 1) + 2, the same columns
+  const uint32_t snd = __builtin_amdgcn_perm(c, a, t.sel_s);
+  const uint32_t r = static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(snd), 0xB1, 0xF, 0xF, false));
+  return as_half4(__builtin_amdgcn_perm(r, a, t.sel_0), __builtin_amdgcn_perm(r, c, t.sel_1));
+}
+
+// PV of step S (lane = dim): the step's values transposed in the lane quads
+// (with MASK, rows past the split end zeroed first: the cache there may hold
+// anything), then one MFMA per half of the dims and query set.
+template <int NSET, bool MASK, int S>
+__device__ __forceinline__ void f16_pv_step(const uint2 (&vc)[32], const QuadT16& qt, int lane, int t0, int t_end,
+                                            const half4_t (&pp)[NSET], float4_t (&O)[NSET][2]) {
+  // before the transpose lane 4b + j holds token 4 S + j of its dims
+  const bool dead = MASK && t0 + 4 * S + (lane & 3) >= t_end;
+  half4_t vv[2];
 #pragma unroll
-  for (int s = 0; s < 8; ++s)
+  for (int h = 0; h < 2; ++h) {
+    uint2 w = vc[2 * S + h];
+    if (MASK) w = dead ? make_uint2(0u, 0u) : w;
+    vv[h] = quad_t16(w, qt);
+  }
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const _Float16* p = vb + static_cast<size_t>(t0 + 4 * (S0 + s)) * kHeadDim + 64 * h + lane;
-      half4_t v;
-      v[0] = p[0];
-      v[1] = p[kHeadDim];
-      v[2] = p[2 * kHeadDim];
-      v[3] = p[3 * kHeadDim];
-      vv[s][h] = v;
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int q = 0; q < NSET; ++q)
+      O[q][h] = __builtin_amdgcn_mfma_f32_4x4x4f16(pp[q], vv[h], O[q][h], 4, S % 16, 0);
+}
+template <int NSET, bool MASK, int S0, int... J>
+__device__ __forceinline__ void f16_pv(std::integer_sequence<int, J...>, const uint2 (&vc)[32], const QuadT16& qt,
+                                       int lane, int t0, int t_end, const half4_t (&pp)[NSET],
+                                       float4_t (&O)[NSET][2]) {
+  (f16_pv_step<NSET, MASK, S0 + J>(vc, qt, lane, t0, t_end, pp, O), ...);
+}
+// PV of a whole tile; the values of the next tile's second half are issued
+// between the two halves.
+template <int NSET, bool MASK>
+__device__ __forceinline__ void f16_pv_tile(const _Float16* vb, int tn, const uint2 (&vc)[32], uint2 (&vn)[32],
+                                            const QuadT16& qt, int lane, int t0, int t_end,
+                                            const half4_t (&pp)[NSET], float4_t (&O)[NSET][2]) {
+  f16_pv<NSET, MASK, 0>(std::make_integer_sequence<int, 8>{}, vc, qt, lane, t0, t_end, pp, O);
+  __builtin_amdgcn_sched_barrier(0);
+  f16_load_values<8>(vb, tn, lane, vn);
+  __builtin_amdgcn_sched_barrier(0);
+  f16_pv<NSET, MASK, 8>(std::make_integer_sequence<int, 8>{}, vc, qt, lane, t0, t_end, pp, O);
+}
+
+// One 64-row tile at t0 (keys in kc, values in vc), with the loads of the tile
+// at tn issued into kn and vn, each half as soon as the registers it replaces
+// in the other set are consumed.
+template <int NSET>
+__device__ __forceinline__ void f16_tile(const uint8_t* smem, const _Float16* kb, const _Float16* vb, int t0, int tn,
+                                         int t_end, int lane, uint32_t qlane, const QuadT16& qt, uint4 (&kc)[16],
+                                         uint2 (&vc)[32], uint4 (&kn)[16], uint2 (&vn)[32], float (&m_run)[NSET],
+                                         float (&l_run)[NSET], float4_t (&O)[NSET][2]) {
+  // sched_barrier(0) keeps each prefetch between the products it was placed
+  // after and before: hoisted further, the loads would hold registers that
+  // the current tile still needs
+  __builtin_amdgcn_s_setprio(2);
+  f16_load_keys<0>(kb, tn, lane, kn);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---------------- QK (lane = token), 32 steps
+  float4_t L[NSET];
+#pragma unroll
+  for (int s = 0; s < NSET; ++s) L[s] = float4_t{0.f, 0.f, 0.f, 0.f};
+  half4_t qh[NSET], ql[NSET];
+#pragma unroll
+  for (int slot = 0; slot < 2; ++slot) {
+#pragma unroll
+    for (int s = 0; s < NSET; ++s) {
+      const uint32_t base = qlane + ((slot * 2 + s) * 2) * 64 * 8;
+      const uint2 uh = lds64(smem, base), ul = lds64(smem, base + 64 * 8);
+      qh[s] = as_half4(uh.x, uh.y);
+      ql[s] = as_half4(ul.x, ul.y);
     }
+    f16_qk_chunk<NSET, 0>(std::make_integer_sequence<int, 8>{}, kc + 8 * slot, qh, ql, L);
+    f16_qk_chunk<NSET, 8>(std::make_integer_sequence<int, 8>{}, kc + 8 * slot + 4, qh, ql, L);
+    __builtin_amdgcn_sched_barrier(0);
+    if (slot == 0) f16_load_keys<8>(kb, tn, lane, kn);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  f16_load_values<0>(vb, tn, lane, vn);
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_setprio(0);
+
+  // ---------------- online softmax, as in the packed decode
+  const bool full = t0 + 64 <= t_end;
+  const int tk = t0 + lane;
+  half4_t pp[NSET];
+#pragma unroll
+  for (int s = 0; s < NSET; ++s) {
+    float4_t x = L[s];
+    if (!full && tk >= t_end) x = float4_t{kNegInf, kNegInf, kNegInf, kNegInf};
+    quad_transpose(x, lane);
+    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    mx = xmax16(mx);
+    const float mn = fmaxf(m_run[s], mx);
+    const float corr = m_run[s] == kNegInf ? 0.f : exp2_hw(m_run[s] - mn);
+    float ps = 0.f;
+    half4_t ph;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float p = exp2_hw(x[r] - mn);
+      ps += p;
+      ph[r] = static_cast<_Float16>(p);
+    }
+    pp[s] = ph;
+    l_run[s] = l_run[s] * corr + ps;
+    if (__builtin_amdgcn_ballot_w64(mn != m_run[s]) != 0) {
+      const float c0 = qperm<0x00>(corr), c1 = qperm<0x55>(corr), c2 = qperm<0xAA>(corr), c3 = qperm<0xFF>(corr);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        O[s][h][0] *= c0;
+        O[s][h][1] *= c1;
+        O[s][h][2] *= c2;
+        O[s][h][3] *= c3;
+      }
+    }
+    m_run[s] = mn;
+  }
+
+  // ---------------- PV (lane = dim), 16 steps of 4 tokens
+  __builtin_amdgcn_s_setprio(1);
+  if (full) f16_pv_tile<NSET, false>(vb, tn, vc, vn, qt, lane, t0, t_end, pp, O);
+  else f16_pv_tile<NSET, true>(vb, tn, vc, vn, qt, lane, t0, t_end, pp, O);
+  __builtin_amdgcn_s_setprio(0);
 }
 
 template <int NSET>
-__global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __restrict__ q,
-                                                       const int32_t* __restrict__ ctx_len,
-                                                       const _Float16* __restrict__ k16,
-                                                       const _Float16* __restrict__ v16, float* __restrict__ out,
-                                                       int32_t* __restrict__ counters, float* __restrict__ part,
-                                                       int n_splits, int split_len) {
+__global__ __launch_bounds__(kF16Threads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_f16_mfma(Dims d, const void* __restrict__ q,
+                                                          const int32_t* __restrict__ ctx_len,
+                                                          const _Float16* __restrict__ k16,
+                                                          const _Float16* __restrict__ v16, float* __restrict__ out,
+                                                          int32_t* __restrict__ counters, float* __restrict__ part,
+                                                          int n_splits, int split_len) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kF16Lds];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1153,7 +1296,7 @@ __global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __res
   // query image, 2 slots of 16 steps (as in the packed decode), logits in
   // base-2 units: q / sqrt(d_h) * log2 e, fp16 hi and lo parts
   static_assert(2 * 2 * 2 * 64 * 8 <= kF16Flag, "query image inside the merge area");
-  for (int i = tid; i < 2 * NSET * 64 * 4; i += kThreads) {
+  for (int i = tid; i < 2 * NSET * 64 * 4; i += kF16Threads) {
     const int k = i & 3, l = (i >> 2) & 63, set = (i >> 8) % NSET, slot = (i >> 8) / NSET;
     const int step = 16 * slot + (l >> 2), qh = 4 * set + (l & 3), coord = 4 * step + k;
     float v = 0.f;
@@ -1175,6 +1318,7 @@ __global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __res
   const _Float16* kb = k16 + row * cap * kHeadDim;
   const _Float16* vb = v16 + row * cap * kHeadDim;
   const uint32_t qlane = static_cast<uint32_t>(lane) * 8;
+  const QuadT16 qt = quad_t16_setup(lane);
 
   float m_run[NSET], l_run[NSET];
   float4_t O[NSET][2];
@@ -1184,118 +1328,39 @@ __global__ __launch_bounds__(kThreads) void k_f16_mfma(Dims d, const void* __res
     l_run[s] = 0.f;
     O[s][0] = O[s][1] = float4_t{0.f, 0.f, 0.f, 0.f};
   }
-  const int stride = kWaves * 64;
-  for (int t0 = t_begin + wave * 64; t0 < t_end; t0 += stride) {
-    // wave priorities as in the packed decode: loads and QK 2, PV 1, softmax 0
-    __builtin_amdgcn_s_setprio(2);
-    // every row of the tile is below the capacity (a multiple of 64)
-    const uint4* kr = reinterpret_cast<const uint4*>(kb + static_cast<size_t>(t0 + lane) * kHeadDim);
-    uint4 ka[4], kn[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) ka[j] = kr[j];
-    half4_t va[8][2];
-    f16_load_values<0>(vb, t0, lane, va);
-
-    // ---------------- QK (lane = token), 4 chunks of 8 steps
-    float4_t L[NSET];
-#pragma unroll
-    for (int s = 0; s < NSET; ++s) L[s] = float4_t{0.f, 0.f, 0.f, 0.f};
-    half4_t qh[NSET], ql[NSET];
-    const auto qslot = [&](int slot) {
-#pragma unroll
-      for (int s = 0; s < NSET; ++s) {
-        const uint32_t base = qlane + ((slot * 2 + s) * 2) * 64 * 8;
-        const uint2 uh = lds64(smem, base), ul = lds64(smem, base + 64 * 8);
-        qh[s] = as_half4(uh.x, uh.y);
-        ql[s] = as_half4(ul.x, ul.y);
-      }
-    };
-    const auto next = [&](int c) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) kn[j] = kr[4 * c + j];
-    };
-    const auto swap = [&]() {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) ka[j] = kn[j];
-    };
-    qslot(0);
-    next(1);
-    f16_qk_chunk<NSET, 0>(std::make_integer_sequence<int, 8>{}, ka, qh, ql, L);
-    swap();
-    next(2);
-    f16_qk_chunk<NSET, 8>(std::make_integer_sequence<int, 8>{}, ka, qh, ql, L);
-    swap();
-    next(3);
-    qslot(1);
-    f16_qk_chunk<NSET, 16>(std::make_integer_sequence<int, 8>{}, ka, qh, ql, L);
-    swap();
-    f16_qk_chunk<NSET, 24>(std::make_integer_sequence<int, 8>{}, ka, qh, ql, L);
-    half4_t vb2[8][2];
-    f16_load_values<8>(vb, t0, lane, vb2);
-    __builtin_amdgcn_s_setprio(0);
-
-    // ---------------- online softmax, as in the packed decode (value rows
-    // past the split end are zeroed: the cache there may hold anything)
-    const bool full = t0 + 64 <= t_end;
-    const int tk = t0 + lane;
-    if (!full) {
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          if (t0 + 4 * s + r >= t_end) va[s][0][r] = va[s][1][r] = static_cast<_Float16>(0.f);
-          if (t0 + 4 * (8 + s) + r >= t_end) vb2[s][0][r] = vb2[s][1][r] = static_cast<_Float16>(0.f);
-        }
-    }
-    half4_t pp[NSET];
-#pragma unroll
-    for (int s = 0; s < NSET; ++s) {
-      float4_t x = L[s];
-      if (!full && tk >= t_end) x = float4_t{kNegInf, kNegInf, kNegInf, kNegInf};
-      quad_transpose(x, lane);
-      float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-      mx = xmax16(mx);
-      const float mn = fmaxf(m_run[s], mx);
-      const float corr = m_run[s] == kNegInf ? 0.f : exp2_hw(m_run[s] - mn);
-      float ps = 0.f;
-      half4_t ph;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = exp2_hw(x[r] - mn);
-        ps += p;
-        ph[r] = static_cast<_Float16>(p);
-      }
-      pp[s] = ph;
-      l_run[s] = l_run[s] * corr + ps;
-      if (__builtin_amdgcn_ballot_w64(mn != m_run[s]) != 0) {
-        const float c0 = qperm<0x00>(corr), c1 = qperm<0x55>(corr), c2 = qperm<0xAA>(corr), c3 = qperm<0xFF>(corr);
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          O[s][h][0] *= c0;
-          O[s][h][1] *= c1;
-          O[s][h][2] *= c2;
-          O[s][h][3] *= c3;
-        }
-      }
-      m_run[s] = mn;
-    }
-
-    // ---------------- PV (lane = dim), 16 steps of 4 tokens
-    __builtin_amdgcn_s_setprio(1);
-    f16_pv<NSET, 0>(std::make_integer_sequence<int, 8>{}, va, pp, O);
-    f16_pv<NSET, 8>(std::make_integer_sequence<int, 8>{}, vb2, pp, O);
-    __builtin_amdgcn_s_setprio(0);
+  // Every tile loaded lies below the capacity (a multiple of 64): a tile past
+  // the split end (the prefetch after the last one, or a wave with no tile)
+  // reloads the current tile or row 0 instead.
+  constexpr int stride = kF16Waves * 64;
+  int t0 = t_begin + wave * 64;
+  uint4 kA[16], kB[16];
+  uint2 vA[32], vB[32];
+  {
+    const int tl = t0 < t_end ? t0 : 0;
+    f16_load_keys<0>(kb, tl, lane, kA);
+    f16_load_keys<8>(kb, tl, lane, kA);
+    f16_load_values<0>(vb, tl, lane, vA);
+    f16_load_values<8>(vb, tl, lane, vA);
+  }
+  while (t0 < t_end) {
+    int tn = t0 + stride < t_end ? t0 + stride : t0;
+    f16_tile<NSET>(smem, kb, vb, t0, tn, t_end, lane, qlane, qt, kA, vA, kB, vB, m_run, l_run, O);
+    t0 += stride;
+    if (t0 >= t_end) break;
+    tn = t0 + stride < t_end ? t0 + stride : t0;
+    f16_tile<NSET>(smem, kb, vb, t0, tn, t_end, lane, qlane, qt, kB, vB, kA, vA, m_run, l_run, O);
+    t0 += stride;
   }
   __syncthreads();
-  finish_unit<NSET, kWaves>(smem, reinterpret_cast<int*>(smem + kF16Flag), d, G, lz, kvh, split, tid, lane, wave,
-                            m_run, l_run, O, counters, part, n_splits, 1.f, nullptr, out, nullptr);
+  finish_unit<NSET, kF16Waves>(smem, reinterpret_cast<int*>(smem + kF16Flag), d, G, lz, kvh, split, tid, lane,
+                               wave, m_run, l_run, O, counters, part, n_splits, 1.f, nullptr, out, nullptr);
 }
 
 inline hipError_t launch_f16_mfma_impl(const Dims& d, const void* q, const int32_t* ctx_len, const void* k16,
                                        const void* v16, float* out, const DecodeWs& ws, hipStream_t s) {
   dim3 grid(ws.n_splits * d.n_kv * d.batch * d.n_lc);
   const auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, d, q, ctx_len, static_cast<const _Float16*>(k16),
+    hipLaunchKernelGGL(kern, grid, dim3(kF16Threads), 0, s, d, q, ctx_len, static_cast<const _Float16*>(k16),
                        static_cast<const _Float16*>(v16), out, ws.counters, ws.part, ws.n_splits, ws.split_len);
   };
   if (d.group <= 4) go(k_f16_mfma<1>);
