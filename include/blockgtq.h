@@ -78,9 +78,9 @@ typedef struct {
 } bgtq_config;
 
 typedef struct {
-  void* k_codes; /* device, see layout above */
-  void* k_norms;
-  void* v_codes;
+  void* k_codes; /* device, see layout above; each of the four buffers     */
+  void* k_norms; /* 16-byte aligned (EINVAL otherwise: the kernels read    */
+  void* v_codes; /* them with 16-byte loads)                               */
   void* v_norms;
 } bgtq_cache;
 
@@ -154,8 +154,9 @@ int blockgtq_layout_init(const bgtq_config* cfg, const uint8_t* h_k_bits,
  *   [batch][n_new][n_kv_heads][head_dim]  (layer >= 0), or
  *   [n_layers][batch][n_new][n_kv_heads][head_dim]  (layer == -1);
  *   16-byte aligned (EINVAL otherwise).  Appends of up to 4 rows (decode
- *   steps) run one latency-oriented kernel; longer ones (prefill) two fp32
- *   MFMA kernels, keys then values, each a dense 128 x 128 product per row.
+ *   steps) run one latency-oriented kernel; longer ones (prefill) one launch
+ *   of key and value workgroups on fp32 MFMAs, a dense 128 x 128 product
+ *   per row.
  * d_write_pos: int32 [batch]; sequence b's tokens go to rows
  *   d_write_pos[b] .. d_write_pos[b] + n_new - 1.  The caller guarantees
  *   d_write_pos[b] + n_new <= capacity (rows past capacity are not written)
@@ -177,7 +178,10 @@ int blockgtq_quantize_append(const bgtq_config* cfg, const void* d_layout, int32
  *      (layer >= 0) or [n_layers][batch][...][head_dim] (layer == -1);
  *      4-byte aligned (EINVAL otherwise).
  * d_ctx_len: int32 [batch], each in [0, max_ctx]; a sequence with 0 rows
- *      gets an all-zero output.
+ *      gets an all-zero output.  A length outside [0, max_ctx] (it is read on
+ *      the device, so the call cannot reject it) makes that sequence's
+ *      outputs NaN; no row is dropped silently and nothing outside the cache
+ *      is read.
  * max_ctx: host-side upper bound of d_ctx_len (<= capacity), sizes the splits.
  * d_out: float, same shape as d_q.
  * d_workspace / ws_bytes: see blockgtq_workspace_bytes (EWORKSPACE if short;
@@ -290,9 +294,10 @@ int blockgtq_decode_attn_protected(const bgtq_config* cfg, const void* d_layout,
  * d_q_pre: pre-RoPE queries [n_layers][batch][n_kv_heads*group][128],
  * d_k_pre, d_v: [n_layers][batch][1][n_kv_heads][128], all in in_dtype.
  * d_pos: device int32 [batch], the new row's position; the caller keeps
- *      d_pos[b] < capacity (rows past it are not written, the context is
- *      clamped) and max_ctx >= every d_pos[b] + 1 (it sizes the splits;
- *      rows past n_splits x split length are not read).
+ *      d_pos[b] < capacity (rows past it are not written) and max_ctx >=
+ *      every d_pos[b] + 1 (it sizes the splits); a sequence whose d_pos[b] + 1
+ *      exceeds max_ctx, or whose d_pos[b] is negative, gets NaN outputs, as in
+ *      blockgtq_decode_attn.
  * rope_base: theta base, finite and > 1 (EINVAL otherwise).
  * d_out: float [n_layers][batch][n_kv_heads*group][128].
  * d_workspace: blockgtq_rope_step_workspace_bytes; its first part is a

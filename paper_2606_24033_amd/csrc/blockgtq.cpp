@@ -199,6 +199,12 @@ Dims dims_of(const bgtq_config* c, int layer) {
   d.in_dtype = c->in_dtype;
   d.layer = layer;
   d.n_lc = layer < 0 ? c->n_layers : 1;
+  d.max_ctx = c->capacity;
+  return d;
+}
+Dims dims_of(const bgtq_config* c, int layer, int max_ctx) {
+  Dims d = dims_of(c, layer);
+  d.max_ctx = max_ctx;
   return d;
 }
 
@@ -242,6 +248,12 @@ SplitPlan plan_splits(const bgtq_config* c, int n_lc, int max_ctx, int requested
 }
 
 size_t al256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+// The kernels read the cache with 16-byte loads.
+bool cache_aligned(const bgtq_cache* c) {
+  const auto a = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
+  return a(c->k_codes) && a(c->k_norms) && a(c->v_codes) && a(c->v_norms);
+}
 
 // Workspace: split counters [n_lc][batch][n_kv] int32, then the split
 // partials [n_lc][batch][Hq][n_splits][130] fp32.
@@ -550,6 +562,7 @@ int blockgtq_quantize_append(const bgtq_config* cfg, const void* d_layout, int32
   if (!d_layout || !d_write_pos || !cache || !cache->k_codes || !cache->k_norms || !cache->v_codes ||
       !cache->v_norms)
     return fail(BGTQ_EINVAL, "NULL pointer");
+  if (!cache_aligned(cache)) return fail(BGTQ_EINVAL, "cache buffers must be 16-byte aligned");
   if (layer < -1 || layer >= cfg->n_layers) return fail(BGTQ_EINVAL, "layer %d out of range", layer);
   if (n_new < 0) return fail(BGTQ_EINVAL, "n_new %d < 0", n_new);
   if (n_new > cfg->capacity) return fail(BGTQ_ECAPACITY, "n_new %d > capacity %d", n_new, cfg->capacity);
@@ -593,9 +606,10 @@ int blockgtq_decode_attn(const bgtq_config* cfg, const void* d_layout, int32_t l
     return e;
   if (!d_layout || !cache || !cache->k_codes || !cache->k_norms || !cache->v_codes || !cache->v_norms)
     return fail(BGTQ_EINVAL, "NULL pointer");
+  if (!cache_aligned(cache)) return fail(BGTQ_EINVAL, "cache buffers must be 16-byte aligned");
   CachePtrs c{static_cast<uint32_t*>(cache->k_codes), static_cast<uint16_t*>(cache->k_norms),
               static_cast<uint32_t*>(cache->v_codes), static_cast<uint16_t*>(cache->v_norms)};
-  hipError_t e = launch_decode_packed(dims_of(cfg, layer), d_layout, d_q, d_ctx_len, c, d_out, ws,
+  hipError_t e = launch_decode_packed(dims_of(cfg, layer, max_ctx), d_layout, d_q, d_ctx_len, c, d_out, ws,
                                       static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "decode_attn launch");
   return ok();
@@ -622,12 +636,13 @@ int blockgtq_decode_attn_noalloc(const bgtq_config* cfg, const void* d_layout, i
     return rc;
   if (!d_layout || !cache || !cache->k_codes || !cache->k_norms || !cache->v_codes || !cache->v_norms)
     return fail(BGTQ_EINVAL, "NULL pointer");
+  if (!cache_aligned(cache)) return fail(BGTQ_EINVAL, "cache buffers must be 16-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
   e = launch_clear_counters(ws.counters, n_lc * cfg->batch * cfg->n_kv_heads, s);
   if (e != hipSuccess) return hip_fail(e, "clear_counters launch");
   CachePtrs c{static_cast<uint32_t*>(cache->k_codes), static_cast<uint16_t*>(cache->k_norms),
               static_cast<uint32_t*>(cache->v_codes), static_cast<uint16_t*>(cache->v_norms)};
-  e = launch_decode_packed(dims_of(cfg, layer), d_layout, d_q, d_ctx_len, c, d_out, ws, s);
+  e = launch_decode_packed(dims_of(cfg, layer, max_ctx), d_layout, d_q, d_ctx_len, c, d_out, ws, s);
   if (e != hipSuccess) return hip_fail(e, "decode_attn_noalloc launch");
   return ok();
 }
@@ -639,7 +654,7 @@ int blockgtq_decode_attn_fp16(const bgtq_config* cfg, int32_t layer, const void*
   if (int e = check_decode_args(cfg, layer, d_q, d_ctx_len, max_ctx, d_out, d_workspace, ws_bytes, n_splits, &ws))
     return e;
   if (!d_k16 || !d_v16) return fail(BGTQ_EINVAL, "NULL pointer");
-  hipError_t e = launch_decode_fp16(dims_of(cfg, layer), d_q, d_ctx_len, d_k16, d_v16, d_out, ws,
+  hipError_t e = launch_decode_fp16(dims_of(cfg, layer, max_ctx), d_q, d_ctx_len, d_k16, d_v16, d_out, ws,
                                     static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "decode_attn_fp16 launch");
   return ok();
@@ -696,6 +711,7 @@ int blockgtq_decode_attn_protected(const bgtq_config* cfg, const void* d_layout,
   if (!d_layout || (!d_window && n_sink + n_recent > 0) || !cache || !cache->k_codes || !cache->k_norms ||
       !cache->v_codes || !cache->v_norms)
     return fail(BGTQ_EINVAL, "NULL pointer");
+  if (!cache_aligned(cache)) return fail(BGTQ_EINVAL, "cache buffers must be 16-byte aligned");
   const int n_lc = layer < 0 ? cfg->n_layers : 1;
   size_t need = 0;
   blockgtq_protected_workspace_bytes(cfg, n_lc, n_splits, max_ctx, &need);
@@ -705,7 +721,7 @@ int blockgtq_decode_attn_protected(const bgtq_config* cfg, const void* d_layout,
   ws.wpart = wpart;
   ws.n_sink = n_sink;
   ws.n_recent = n_recent;
-  const Dims d = dims_of(cfg, layer);
+  const Dims d = dims_of(cfg, layer, max_ctx);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = launch_window_attn(d, d_q, d_ctx_len, static_cast<const _Float16*>(d_window), n_sink, n_recent,
                                     wpart, s);
@@ -753,6 +769,7 @@ int blockgtq_rope_decode_step(const bgtq_config* cfg, const void* d_layout, doub
   if (!d_layout || !d_q_pre || !d_k_pre || !d_v || !d_pos || !d_out || !d_workspace || !cache || !cache->k_codes ||
       !cache->k_norms || !cache->v_codes || !cache->v_norms)
     return fail(BGTQ_EINVAL, "NULL pointer");
+  if (!cache_aligned(cache)) return fail(BGTQ_EINVAL, "cache buffers must be 16-byte aligned");
   if (!(rope_base > 1.0) || !std::isfinite(rope_base)) return fail(BGTQ_EINVAL, "rope_base must be finite and > 1");
   if (n_splits < 0 || n_splits > 4096) return fail(BGTQ_EINVAL, "n_splits %d outside 0..4096", n_splits);
   if (max_ctx < 1 || max_ctx > cfg->capacity) return fail(BGTQ_ECAPACITY, "max_ctx %d outside [1, capacity]", max_ctx);
@@ -763,7 +780,7 @@ int blockgtq_rope_decode_step(const bgtq_config* cfg, const void* d_layout, doub
   float* qo = reinterpret_cast<float*>(base + w.q);
   float* ko = reinterpret_cast<float*>(base + w.k);
   float* vo = reinterpret_cast<float*>(base + w.v);
-  Dims d = dims_of(cfg, -1);
+  Dims d = dims_of(cfg, -1, max_ctx);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = launch_rope_step(d, rope_base, d_q_pre, d_k_pre, d_v, d_pos, qo, ko, vo, ctx, s);
   if (e != hipSuccess) return hip_fail(e, "rope_step launch");
@@ -801,6 +818,7 @@ int blockgtq_prefill_attn(const bgtq_config* cfg, const void* d_layout, int32_t 
   if (!d_layout || !d_q || !d_q_pos0 || !d_out || !d_workspace || !cache || !cache->k_codes || !cache->k_norms ||
       !cache->v_codes || !cache->v_norms)
     return fail(BGTQ_EINVAL, "NULL pointer");
+  if (!cache_aligned(cache)) return fail(BGTQ_EINVAL, "cache buffers must be 16-byte aligned");
   if (reinterpret_cast<uintptr_t>(d_q) % 4 != 0) return fail(BGTQ_EINVAL, "q must be 4-byte aligned");
   if (max_pos < 0 || max_pos >= cfg->capacity)
     return fail(BGTQ_ECAPACITY, "max_pos %d outside [0, capacity)", max_pos);

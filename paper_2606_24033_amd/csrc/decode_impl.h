@@ -67,6 +67,13 @@ constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLog2e = 1.4426950408889634f;
 // 2^x (the hardware exponential; arguments here are <= 0)
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+// A quiet NaN the compiler cannot see (these files are built assuming no
+// NaNs): the output scale of a sequence whose context length is out of range.
+__device__ __forceinline__ float opaque_nan() {
+  uint32_t b = 0x7FC00000u;
+  asm volatile("" : "+v"(b));
+  return __uint_as_float(b);
+}
 // fp16(p0 lo(w)) | fp16(p1 hi(w)) << 16, w = two fp16: one mixed-precision
 // fused product into each half (single rounding to fp16)
 __device__ __forceinline__ uint32_t mix_pair(float p0, float p1, uint32_t w) {
@@ -618,7 +625,7 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
     if (n_splits == 1) {
       float e = 0.f;
       if (wpart != nullptr) e = merge_window(wpart + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * 130, mx, l, a);
-      os[i] = l > 0.f ? a / l * oscale : 0.f;
+      os[i] = (l > 0.f ? a / l : 0.f) * oscale;  // oscale NaN: flagged sequence
       if (wpart != nullptr) ws_[i] = l > 0.f ? e / l : 0.f;
     } else {
       // agent-scope stores: written through to the device coherence point
@@ -697,7 +704,7 @@ __device__ __forceinline__ void finish_unit(uint8_t* smem, int* last, const Dims
       }
       float e = 0.f;
       if (wpart != nullptr) e = merge_window(wpart + (static_cast<size_t>(lz) * hqn + kvh * G + qh) * 130, mx, l, a);
-      os[i] = l > 0.f ? a / l * oscale : 0.f;
+      os[i] = (l > 0.f ? a / l : 0.f) * oscale;  // oscale NaN: flagged sequence
       if (wpart != nullptr) ws_[i] = l > 0.f ? e / l : 0.f;
     }
     if (tid == 0) __hip_atomic_store(counters + lz * d.n_kv + kvh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -930,7 +937,11 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
   // address stays (shifted field & mask) | base, one and-or
   asm volatile("" : "+v"(rep.r1), "+v"(rep.r3), "+v"(rep.r4), "+v"(rep.r5), "+v"(rep.r2), "+v"(rep.r1b));
 
-  const int ctx = min(ctx_len[seq], cap);
+  // a context length outside [0, max_ctx] (the host's bound, which sized
+  // the splits) makes the sequence's outputs NaN instead of dropping rows
+  const int ctx_raw = ctx_len[seq];
+  const bool ctx_ok = ctx_raw >= 0 && ctx_raw <= d.max_ctx;
+  const int ctx = min(ctx_raw, cap);
   // packed rows [t_lo, t_hi): all of them, or those between the protected
   // window's sink and recent rows (none when the window covers the context;
   // t_lo < 64, so the first tile of a non-empty range holds a row of it)
@@ -1078,7 +1089,8 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
   }
 
   finish_unit<NSET, kWaves>(smem, reinterpret_cast<int*>(smem + kGmeta), d, G, lz, kvh, split, tid, lane, wave,
-                            m_run, l_run, O, counters, part, n_splits, 0.08838834764831845f /* 1/sqrt(d_h) */,
+                            m_run, l_run, O, counters, part, n_splits,
+                            ctx_ok ? 0.08838834764831845f /* 1/sqrt(d_h) */ : opaque_nan(),
                             reinterpret_cast<const float*>(blob + kOffRotV), out, win.part);
 }
 
@@ -1311,7 +1323,9 @@ __global__ __launch_bounds__(kF16Threads) __attribute__((amdgpu_waves_per_eu(1, 
   }
   __syncthreads();
 
-  const int ctx = min(ctx_len[seq], cap);
+  const int ctx_raw = ctx_len[seq];
+  const bool ctx_ok = ctx_raw >= 0 && ctx_raw <= d.max_ctx;  // else NaN outputs, as in the packed decode
+  const int ctx = min(ctx_raw, cap);
   const int t_begin = split * split_len;
   const int t_end = min(t_begin + split_len, ctx);
   const size_t row = (static_cast<size_t>(layer) * d.batch + seq) * d.n_kv + kvh;
@@ -1353,7 +1367,8 @@ __global__ __launch_bounds__(kF16Threads) __attribute__((amdgpu_waves_per_eu(1, 
   }
   __syncthreads();
   finish_unit<NSET, kF16Waves>(smem, reinterpret_cast<int*>(smem + kF16Flag), d, G, lz, kvh, split, tid, lane,
-                               wave, m_run, l_run, O, counters, part, n_splits, 1.f, nullptr, out, nullptr);
+                               wave, m_run, l_run, O, counters, part, n_splits, ctx_ok ? 1.f : opaque_nan(),
+                               nullptr, out, nullptr);
 }
 
 inline hipError_t launch_f16_mfma_impl(const Dims& d, const void* q, const int32_t* ctx_len, const void* k16,

@@ -10,6 +10,7 @@ struct Dims {
   int n_layers, batch, n_kv, group, capacity, k_words, v_bits, in_dtype;
   int layer;      // >= 0: one layer; -1: all layers
   int n_lc;       // layers in this call (1 or n_layers)
+  int max_ctx;    // decode calls: the host's bound on ctx_len (outputs of a sequence outside [0, max_ctx] are NaN)
 };
 
 struct CachePtrs {

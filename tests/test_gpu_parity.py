@@ -512,6 +512,42 @@ def test_zero_rows_and_noop_calls():
     assert P.rel_err(out[0].cpu().numpy().astype(np.float64), ref) <= 2e-3
 
 
+def test_out_of_range_context_lengths_give_nan():
+    """A context length outside [0, max_ctx] is read on the device, so the call
+    cannot reject it: that sequence's outputs are NaN (no row is dropped
+    silently), in the packed decode, the no-allocation entry point and the
+    fp16 comparator, while the call's other sequences match the oracle."""
+    bg = bgm()
+    st = P.make_setup(8, 1, 4, 1, 4, 256, 160, 2, 1e4, "fp32", n_cal=64)
+    layout, cache = build(st)
+    T = 200
+    kvs = [[P.keys_values(st, 0, 0, 64 * b, T)] for b in range(4)]
+    append(st, layout, cache, 0, kvs, [0, 0, 0, 0])
+    qs = [synth.cast(synth.queries(8, 0, 0, T, 4, 1e4), "fp32") for _ in range(4)]
+    q = to_dev(np.stack(qs)[:, :, :], "fp32")
+    max_ctx = 130
+    ctx = torch.tensor([120, max_ctx + 1, -1, max_ctx], dtype=torch.int32, device="cuda")
+    k16 = torch.zeros((1, 4, 1, 256, 128), dtype=torch.float16, device="cuda")
+    v16 = torch.zeros_like(k16)
+    for b in range(4):
+        k16[0, b, 0, :T] = torch.from_numpy(kvs[b][0][0].astype(np.float32)).half()
+        v16[0, b, 0, :T] = torch.from_numpy(kvs[b][0][1].astype(np.float32)).half()
+    for n_splits in (0, 1, 3):
+        outs = {"packed": bg.blockgtq_decode_attn(st.cfg, layout, 0, q, ctx, max_ctx, cache, n_splits=n_splits),
+                "noalloc": bg.blockgtq_decode_attn_noalloc(st.cfg, layout, 0, q, ctx, max_ctx, cache,
+                                                           torch.empty(4, 4, 128, device="cuda"), n_splits=n_splits),
+                "fp16": bg.blockgtq_decode_attn_fp16(st.cfg, 0, q, ctx, max_ctx, k16, v16, n_splits=n_splits)}
+        torch.cuda.synchronize()
+        for name, out in outs.items():
+            o_ = out.cpu().numpy()
+            assert np.isnan(o_[1]).all() and np.isnan(o_[2]).all(), (name, n_splits)
+            assert np.isfinite(o_[0]).all() and np.isfinite(o_[3]).all(), (name, n_splits)
+        for b, c in ((0, 120), (3, max_ctx)):
+            rows = P.oracle_rows(st, 0, 0, kvs[b][0][0][:c], kvs[b][0][1][:c])
+            ref = P.oracle_attention(st, 0, 0, qs[b], rows, c)
+            assert P.rel_err(outs["packed"][b].cpu().numpy().astype(np.float64), ref) <= P.tol_attention()
+
+
 def test_argument_errors_on_device():
     bg = bgm()
     st = P.make_setup(7, 1, 1, 1, 4, 64, 192, 3, 1e4, "fp32", n_cal=32)

@@ -214,3 +214,31 @@ def test_bench_refuses_more_than_one_gpu():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_cache_buffers_must_be_16_byte_aligned():
+    """Every entry point that reads or writes the packed cache rejects a cache
+    buffer that is not 16-byte aligned (the kernels use 16-byte loads) before
+    any launch: the fake pointers are never dereferenced."""
+    cfg = bg.Config(n_layers=1, batch=1, n_kv_heads=1, group=4, capacity=128, k_budget=128, v_bits=2)
+    L = bg.lib()
+    c = cfg.c()
+    f = ctypes.c_void_p(256)
+    big = 1 << 30
+    for field in ("k_codes", "k_norms", "v_codes", "v_norms"):
+        ptrs = dict(k_codes=256, k_norms=256, v_codes=256, v_norms=256)
+        ptrs[field] = 264
+        cache = ctypes.byref(bg._Cache(**ptrs))
+        calls = {
+            "quantize_append": lambda: L.blockgtq_quantize_append(ctypes.byref(c), f, 0, f, f, 3, f, cache, None),
+            "decode_attn": lambda: L.blockgtq_decode_attn(ctypes.byref(c), f, 0, f, f, 10, cache, f, f, big, 0, None),
+            "decode_attn_protected": lambda: L.blockgtq_decode_attn_protected(ctypes.byref(c), f, 0, f, f, 10, cache,
+                                                                              f, 4, 8, f, f, big, 0, None),
+            "rope_decode_step": lambda: L.blockgtq_rope_decode_step(ctypes.byref(c), f, 1e4, f, f, f, f, 10, cache,
+                                                                    f, f, big, 0, None),
+            "prefill_attn": lambda: L.blockgtq_prefill_attn(ctypes.byref(c), f, 0, f, 10, f, 100, cache, f, f, big,
+                                                            None),
+        }
+        for name, call in calls.items():
+            assert call() == -1, (field, name)
+            assert b"16-byte aligned" in L.blockgtq_last_error(), (field, name)
