@@ -53,7 +53,7 @@ constexpr float kNegInf = -__builtin_huge_valf();
 
 // ---- LDS map of the attention kernel (bytes)
 constexpr int kKStride = 136;  // halves per decoded key row (128 + 8 pad)
-constexpr int kVStride = 72;   // halves per decoded value row (64 + 8 pad)
+constexpr int kVStride = 68;   // halves per decoded value row (64 + 4 pad: conflict-free stores and PV reads)
 // decoded tile (two buffers): key hi, key lo [64 tokens][kKStride] fp16,
 // values [128 dims][kVStride] fp16, value radii [64] fp16
 constexpr int kDecKH = 0;
@@ -62,10 +62,12 @@ constexpr int kDecV = kDecKL + 64 * kKStride * 2;
 constexpr int kDecVN = kDecV + 128 * kVStride * 2;
 constexpr int kDecBytes = kDecVN + 64 * 2;
 // raw tile (two buffers): key words [64][k_words], value words [2 value
-// tiles][128 dims][b_V], key radii [64][8] fp16, value radii [64] fp16
+// tiles][128 dims][b_V] (the second tile kRawV1 words further), key radii
+// [64][8] fp16, value radii [64] fp16
 constexpr int kRawK = 0;
 constexpr int kRawV = kRawK + 64 * kMaxKWords * 4;
-constexpr int kRawKN = kRawV + 2 * kHeadDim * 8 * 4;
+constexpr int kRawV1 = 4;  // words between the two value tiles: their same dims on other banks
+constexpr int kRawKN = kRawV + (2 * kHeadDim * 8 + kRawV1) * 4;
 constexpr int kRawVN = kRawKN + 64 * 8 * 2;
 constexpr int kRawBytes = kRawVN + 64 * 2;
 constexpr int kOffDec = 0;
@@ -250,7 +252,8 @@ template <int E0>
 __device__ __forceinline__ void decode_values(const uint8_t* smem, const uint8_t* raw, uint8_t* dec, int tid,
                                               int bv) {
   const int vd = tid / kVGrp, vq = (tid % kVGrp) * kVPer + E0;
-  const uint32_t* vr = reinterpret_cast<const uint32_t*>(raw + kRawV) + ((vq / kTile) * kHeadDim + vd) * bv;
+  const uint32_t* vr =
+      reinterpret_cast<const uint32_t*>(raw + kRawV) + ((vq / kTile) * kHeadDim + vd) * bv + (vq / kTile) * kRawV1;
   const uint16_t* cb = reinterpret_cast<const uint16_t*>(smem + kOffCb) + cb_index(bv);
   const uint32_t mask = (1u << bv) - 1u;
   half8_t hv;
@@ -261,7 +264,11 @@ __device__ __forceinline__ void decode_values(const uint8_t* smem, const uint8_t
     const uint32_t code = __builtin_amdgcn_alignbit(vr[w + 1], vr[w], bit & 31u) & mask;
     hv[e] = __builtin_bit_cast(_Float16, cb[code]);
   }
-  *reinterpret_cast<half8_t*>(reinterpret_cast<_Float16*>(dec + kDecV) + vd * kVStride + vq) = hv;
+  // two 8-byte stores: the row stride keeps only 8-byte alignment
+  uint2* dst = reinterpret_cast<uint2*>(reinterpret_cast<_Float16*>(dec + kDecV) + vd * kVStride + vq);
+  const uint4 hb = __builtin_bit_cast(uint4, hv);
+  dst[0] = make_uint2(hb.x, hb.y);
+  dst[1] = make_uint2(hb.z, hb.w);
   if (E0 == 0 && tid < kKeyTile)
     reinterpret_cast<uint16_t*>(dec + kDecVN)[tid] = reinterpret_cast<const uint16_t*>(raw + kRawVN)[tid];
 }
@@ -487,7 +494,7 @@ __global__ __launch_bounds__(kAttnThreads) void k_prefill_attn(
     for (int j = 0; j < kRawPer; ++j) {
       const int i = tid + j * kAttnThreads;
       if (i < nk4) reinterpret_cast<uint4*>(raw + kRawK)[i] = pk[j];
-      if (i < nv4) reinterpret_cast<uint4*>(raw + kRawV)[i] = pv[j];
+      if (i < nv4) reinterpret_cast<uint4*>(raw + kRawV)[i + (4 * i >= kHeadDim * bv ? kRawV1 / 4 : 0)] = pv[j];
       if (i < nkn) reinterpret_cast<uint16_t*>(raw + kRawKN)[(i / nslot) * 8 + i % nslot] = pkn[j];
     }
     if (tid < kKeyTile) reinterpret_cast<uint16_t*>(raw + kRawVN)[tid] = pvn;
