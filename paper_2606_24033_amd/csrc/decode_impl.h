@@ -3,8 +3,10 @@
 // products -> online softmax over a split of the key axis, then the exact
 // log-sum-exp merge of the splits and the inverse V rotation).
 //
-// Work mapping.  One workgroup = 16 waves (one per CU) = one (split, KV
-// head, sequence[, layer]).  A wave owns 64-token tiles (two value tiles).  Both products run
+// Work mapping.  One workgroup (one per CU: the lookup tables fill its LDS;
+// 16 waves for up to 4 query heads per KV head, 12 for 5-8) = one (split,
+// KV head, sequence[, layer]).  A wave owns 64-token tiles (two value
+// tiles).  Both products run
 // on 4x4x4 f16 MFMA instructions (16 independent 4x4 blocks) whose A operand
 // is broadcast from one block (CBSZ = 4, ABID = the block), so the operand
 // shared by all 64 lanes is held once per 16 steps instead of once per step:
@@ -54,7 +56,7 @@ namespace split_detail {
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 16;  // one workgroup per CU: 160 KB of LDS for the tables
+constexpr int kWaves = 16;  // the 16-wave workgroup (merge-area sizes, the one-set decode)
 constexpr int kThreads = kWaves * 64;
 // Waves of a packed-decode workgroup: 16 (4 per SIMD) with one query set;
 // 12 with two (3 per SIMD, up to 168 VGPRs for the doubled accumulators:
@@ -730,7 +732,7 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
     Dims d, const uint8_t* __restrict__ blob, const void* __restrict__ q, const int32_t* __restrict__ ctx_len,
     CachePtrs c, float* __restrict__ out, int32_t* __restrict__ counters, float* __restrict__ part, int n_splits,
     int split_len, WinArgs win) {
-  // this instantiation's workgroup (shadows the comparator's 16 waves)
+  // this instantiation's workgroup (shadows the 16-wave default)
   constexpr int kWaves = split_waves<NSET>(), kThreads = kWaves * 64;
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int tid = threadIdx.x, lane = tid & 63;
