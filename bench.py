@@ -18,9 +18,11 @@ The other workloads of the measurement plan are reported beside it (each its
 own sub-object): the toy single head, one Qwen2.5-3B-shaped layer at 32K (the
 prefill call and the median of 64 steps), the Qwen2.5-3B-shaped K3V3 step at
 128K / 256K / 512K rows (with the fp16 comparator and packed-vs-fp16 bytes),
-the ragged batch of 8 (cold and warm), the prefill quantize_append against
-the fp32 roofline, a read-probe ceiling, and the fp64 CPU oracle on the
-host's cores.
+the ragged batch of 8 (cold and warm; the toy head and the 32K layer are
+also timed cold, after a 1 GiB cache flush per step), the prefill
+quantize_append against the fp32 roofline, a read-probe ceiling, the
+headline step as per-layer launches replayed from a HIP graph, and the fp64
+CPU oracle on the host's cores (with the headline's parity statistics).
 
 Prints one JSON line.  The design notes give the roofline definitions.
 """
@@ -321,9 +323,31 @@ def sdpa_decode_context(torch, m, W, K):
         return None
 
 
-def workload_line(torch, m, args, label, settle_s, fp16=False):
-    """Settle, K timed steps, then (fp16) the packed and fp16 decodes
-    interleaved at the timed steps' contexts."""
+def cold_warm_steps(torch, m, first, n, flush_bytes=1 << 30):
+    """Steps first .. first+n-1 again (the same rows at the same positions:
+    the cache content does not change), each twice in a row and timed alike:
+    warm, then after an untimed write of a 1 GiB buffer that evicts the L2
+    and MALL (cold: the step from HBM)."""
+    flush = torch.empty(flush_bytes, dtype=torch.uint8, device="cuda")
+    evw = [ev_pair(torch) for _ in range(n)]
+    evc = [ev_pair(torch) for _ in range(n)]
+    for i in range(n):
+        evw[i][0].record()
+        m.step(first + i)
+        evw[i][1].record()
+        flush.fill_(i & 255)
+        evc[i][0].record()
+        m.step(first + i)
+        evc[i][1].record()
+    torch.cuda.synchronize()
+    del flush
+    return [a.elapsed_time(b) * 1e3 for a, b in evw], [a.elapsed_time(b) * 1e3 for a, b in evc]
+
+
+def workload_line(torch, m, args, label, settle_s, fp16=False, cold=False):
+    """Settle, K timed steps, then (cold) the same steps after a cache flush
+    each, then (fp16) the packed and fp16 decodes interleaved at the timed
+    steps' contexts."""
     W = min(args.warmup, m.n_steps - args.steps)
     for s in range(W):
         m.step(s)
@@ -343,6 +367,11 @@ def workload_line(torch, m, args, label, settle_s, fp16=False):
            "cache_bytes": {"packed": packed, "fp16": f16b, "compression": round(f16b / packed, 3)},
            "prefill_quantize_us": stats([u for u, _ in m.prefill_us]),
            "prefill_rows_per_call": int(m.prefill_us[0][1] * m.H)}
+    if cold:
+        wu, cu = cold_warm_steps(torch, m, W, args.steps)
+        res["flush_ab"] = {"warm_step_us": stats(wu), "cold_step_us": stats(cu),
+                           "cold_step_gbs": round(sb / (np.median(cu) * 1e-6) / 1e9, 2),
+                           "note": "each step timed twice alike: warm, then after a 1 GiB flush"}
     if fp16:
         out16 = torch.empty_like(m.out)
         p_us, f_us = interleaved(torch, [lambda i: m.decode(W + i), lambda i: m.decode_fp16(W + i, out16)],
@@ -462,6 +491,51 @@ def rope_step_measurement(bg, torch, m, args, W):
             "eager_over_post_rope_step": round(float(np.median(e_us) / np.median(p_us)), 3),
             "graph_over_post_rope_step": round(float(np.median(g_us) / np.median(p_us)), 3),
             "kernels": "k_rope_step + k_append_rows + k_split_mfma"}
+
+
+def per_layer_graph_measurement(bg, torch, m, args, W):
+    """The headline step as per-layer launches: for every layer its append and
+    its decode (2 x 32 launches) captured in one HIP graph, replayed with the
+    step's rows, queries and position copied into the captured buffers before
+    each replay, interleaved with the all-layer step (two launches)."""
+    ws1 = torch.zeros(bg.workspace_bytes(m.cfg, 1, m.n_splits, m.max_ctx), dtype=torch.uint8, device="cuda")
+    k_in, v_in, q_in = m.knew[W].clone(), m.vnew[W].clone(), m.q[W].clone()
+    wp, cx = m.wps[W:W + 1].clone(), m.ctxs[W:W + 1].clone()
+    out = torch.empty_like(m.out)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            for layer in range(m.L):
+                bg.blockgtq_quantize_append(m.cfg, m.layout, layer, k_in[layer], v_in[layer], wp, m.cache,
+                                            stream=side)
+                bg.blockgtq_decode_attn(m.cfg, m.layout, layer, q_in[layer], cx, m.max_ctx, m.cache, out=out[layer],
+                                        workspace=ws1, n_splits=m.n_splits, stream=side)
+    torch.cuda.synchronize()
+
+    def replay(i):
+        s = W + i
+        k_in.copy_(m.knew[s])
+        v_in.copy_(m.vnew[s])
+        q_in.copy_(m.q[s])
+        wp.copy_(m.wps[s:s + 1])
+        cx.copy_(m.ctxs[s:s + 1])
+        graph.replay()
+
+    for i in range(max(3, min(args.warmup, 10))):  # the first replays also upload the graph
+        replay(i % args.steps)
+        m.step(W + i % args.steps)
+    torch.cuda.synchronize()
+    a_us, g_us = interleaved(torch, [lambda i: m.step(W + i), replay], args.steps)
+    torch.cuda.synchronize()
+    # the last round's outputs of the two forms (same step; the split plans differ)
+    diff = float(((out - m.out).abs().max() / m.out.abs().max()).item())
+    del graph
+    return {"all_layer_step_us_interleaved": stats(a_us), "per_layer_graph_step_us": stats(g_us),
+            "max_rel_diff_vs_all_layer_step": round(diff, 7),
+            "graph_over_all_layer_step": round(float(np.median(g_us) / np.median(a_us)), 3),
+            "launches": f"graph: {2 * m.L} (append + decode per layer) and 5 input copies; all-layer step: 2"}
 
 
 def prefill_measurement(bg, synth, torch, m, T):
@@ -706,6 +780,37 @@ def _cpu_model():
     return "unknown"
 
 
+def headline_parity(bg, synth, torch, m, units):
+    """Parity statistics of the headline workload, part of the CPU-oracle leg
+    (the only part of this script that calls the oracle): for a few (layer, KV
+    head) units, the fp64 oracle on the same seeded rows (regenerated on the
+    device by the same generator call as the prefill, copied to the host)
+    against the library's decode of the first step (context T + 1), per query
+    head max |out - ref| / max |ref|."""
+    from oracle import blockgtq_oracle as o
+    G, T = m.G, m.T
+    ctx = m.ctxs[0:1].clone()
+    out = torch.empty_like(m.out)
+    bg.blockgtq_decode_attn(m.cfg, m.layout, -1, m.q[0], ctx, m.max_ctx, m.cache, out=out, workspace=m.ws,
+                            n_splits=m.n_splits)
+    torch.cuda.synchronize()
+    errs = []
+    for layer, h in units:
+        k, v = synth.torch_layer_kv(m.seed, layer, m.T + m.n_steps, m.sig[layer], m.base)
+        kk = k[:T + 1, h].float().cpu().numpy()
+        vv = v[:T + 1, h].float().cpu().numpy()
+        del k, v
+        kc, _, kn, _ = o.quantize_keys(kk, m.bits[layer, h], m.rot_k)
+        vc, vn, _ = o.quantize_values(vv, m.rot_v, m.vb)
+        q = m.q[0][layer, 0, h * G:(h + 1) * G].float().cpu().numpy()
+        ref = o.attention_rotated(q, kc, kn, m.bits[layer, h], m.rot_k, vc, vn, m.rot_v, m.vb)
+        got = out[layer, 0, h * G:(h + 1) * G].double().cpu().numpy()
+        errs.append(float(np.max(np.abs(got - ref)) / np.max(np.abs(ref))))
+    return {"units": [list(u) for u in units], "ctx": T + 1, "max_rel_err": round(max(errs), 7),
+            "per_unit": [round(e, 7) for e in errs], "budget": 2e-3,
+            "note": "oracle codes from its own fp64 encode; threshold ties (counted in the tests) are not separated"}
+
+
 def cpu_oracle_baseline(bits, T, workers, spec=LLAMA, budget_s=8.0):
     """The fp64 CPU oracle (rotated form, as it stands) on a bounded sample of
     the headline step: `workers` processes, one host core and one (layer, KV
@@ -835,6 +940,10 @@ def main():
             m, f"prefill quantize_append of {T} rows x 8 KV heads per call (one call per layer), Llama-3.1-8B "
                "shape, K2V2, bf16")
 
+    parity = None
+    if not args.no_cpu and not args.only_headline:
+        parity = headline_parity(bg, synth, torch, m, [(5, 3), (27, 6)])
+        log(f"headline parity {parity['max_rel_err']}")
     if want_fp16:
         out16 = torch.empty_like(m.out)
         p_us, f_us = interleaved(torch, [lambda i: m.decode(W + i), lambda i: m.decode_fp16(W + i, out16)], K)
@@ -859,6 +968,7 @@ def main():
 
     if not args.no_rope_step and not args.only_headline:
         result["rope_step"] = rope_step_measurement(bg, torch, m, args, W)
+        result["per_layer_graph"] = per_layer_graph_measurement(bg, torch, m, args, W)
 
     if not args.no_prefill and not args.only_headline:
         result["prefill_attn"] = prefill_measurement(bg, synth, torch, m, args.prefill_len)
@@ -871,13 +981,14 @@ def main():
         toy = Model(bg, synth, torch, dict(name="toy", seed=1, n_layers=1, n_kv=1, group=4, base=1e4, k_budget=192,
                                            v_bits=2), 2048, W + K, in_dtype=bg.BGTQ_FP32, n_cal=256)
         wl["toy_single_head"] = workload_line(torch, toy, args, "toy single head: 1 layer, 1 KV head, G = 4, "
-                                              "base 1e4, 2048 fp32 rows, K3V2 (latency-bound; report us only)", 0.3)
+                                              "base 1e4, 2048 fp32 rows, K3V2 (latency-bound; report us only)", 0.3,
+                                              cold=True)
         toy.free()
         q2 = Model(bg, synth, torch, dict(name="Qwen2.5-3B", seed=2, n_layers=1, n_kv=2, group=8, base=1e6,
                                           k_budget=192, v_bits=3), 32768, max(64, W + K))
         K64 = argparse.Namespace(**{**vars(args), "steps": 64, "warmup": 0})
         line = workload_line(torch, q2, K64, "Qwen2.5-3B-shaped layer: 16 q / 2 KV heads, base 1e6, bf16, "
-                             "32768 rows, K3V3; 64 decode steps", 0.3)
+                             "32768 rows, K3V3; 64 decode steps", 0.3, cold=True)
         wp0 = torch.zeros(1, dtype=torch.int32, device="cuda")
         kk, vv = synth.torch_layer_kv(2, 0, 32768, q2.sig[0], q2.base)
         kk, vv = kk[None].contiguous(), vv[None].contiguous()
@@ -907,6 +1018,8 @@ def main():
     if not args.no_cpu and not args.only_headline:
         workers = args.cpu_workers or min(16, len(os.sched_getaffinity(0)))
         result["cpu_baseline"] = cpu_oracle_baseline(bits_llama, T, workers, spec)
+        if parity is not None:
+            result["cpu_baseline"]["headline_parity"] = parity
     print(json.dumps(result), flush=True)
 
 
