@@ -146,31 +146,43 @@ __device__ __forceinline__ float qperm(float v) {
 }
 
 // 4x4 transpose inside every lane quad: on entry lane p of a quad holds
-// x[r] = M[r][p]; on exit it holds x[t] = M[p][t].
-__device__ __forceinline__ void quad_transpose(float4_t& x, int lane) {
-  const bool odd = lane & 1, hi2 = lane & 2;
-  {
-    const float n0 = qperm<0xB1>(x[0]), n1 = qperm<0xB1>(x[1]);
-    const float n2 = qperm<0xB1>(x[2]), n3 = qperm<0xB1>(x[3]);
-    if (odd) {
-      x[0] = n1;
-      x[2] = n3;
-    } else {
-      x[1] = n0;
-      x[3] = n2;
-    }
-  }
-  {
-    const float n0 = qperm<0x4E>(x[0]), n1 = qperm<0x4E>(x[1]);
-    const float n2 = qperm<0x4E>(x[2]), n3 = qperm<0x4E>(x[3]);
-    if (hi2) {
-      x[0] = n2;
-      x[1] = n3;
-    } else {
-      x[2] = n0;
-      x[3] = n1;
-    }
-  }
+// x[r] = M[r][p]; on exit it holds x[t] = M[p][t].  Two exchange stages
+// (partner lanes p ^ 1, then p ^ 2); each output element is one select whose
+// other operand is read from the partner lane by DPP (v_cndmask_b32 takes the
+// DPP operand as src0, chosen where the lane mask in vcc is clear).  The
+// s_nop 1 lines give the two wait states a DPP read needs after a VALU
+// write of its operand.
+__device__ __forceinline__ void quad_transpose(float4_t& x, int) {
+  float y0, y1, y2, y3, z0, z1, z2, z3;
+  asm volatile(
+      // stage 1: even lanes take x1, x3 from the odd partner's x0, x2; odd
+      // lanes take x0, x2 from the even partner's x1, x3
+      "s_mov_b32 vcc_lo, 0x55555555\n\t"
+      "s_mov_b32 vcc_hi, 0x55555555\n\t"
+      "s_nop 1\n\t"
+      "v_cndmask_b32_dpp %0, %5, %4, vcc quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_cndmask_b32_dpp %2, %7, %6, vcc quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "s_not_b64 vcc, vcc\n\t"
+      "v_cndmask_b32_dpp %1, %4, %5, vcc quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_cndmask_b32_dpp %3, %6, %7, vcc quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf"
+      : "=&v"(y0), "=&v"(y1), "=&v"(y2), "=&v"(y3)
+      : "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3])
+      : "vcc");
+  asm volatile(
+      // stage 2: lanes 0, 1 of a quad take x2, x3 from partner p + 2's x0,
+      // x1; lanes 2, 3 take x0, x1 from partner p - 2's x2, x3
+      "s_mov_b32 vcc_lo, 0x33333333\n\t"
+      "s_mov_b32 vcc_hi, 0x33333333\n\t"
+      "s_nop 1\n\t"
+      "v_cndmask_b32_dpp %0, %6, %4, vcc quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+      "v_cndmask_b32_dpp %1, %7, %5, vcc quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+      "s_not_b64 vcc, vcc\n\t"
+      "v_cndmask_b32_dpp %2, %4, %6, vcc quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+      "v_cndmask_b32_dpp %3, %5, %7, vcc quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf"
+      : "=&v"(z0), "=&v"(z1), "=&v"(z2), "=&v"(z3)
+      : "v"(y0), "v"(y1), "v"(y2), "v"(y3)
+      : "vcc");
+  x = float4_t{z0, z1, z2, z3};
 }
 
 // Rotate right by N lanes inside every 16-lane row (DPP row_ror).
@@ -541,6 +553,25 @@ __device__ __forceinline__ uint32_t radius_bits(const uint32_t (&knp)[4], int g)
   return knp[g >> 1] >> (16 * (g & 1));
 }
 
+// Radius bits of the group of width BM1 + 1.  Its ordinal is BM1 when every
+// narrower width is present, BM1 - 1 when exactly one is missing (rows whose
+// narrowest width is 2): in the model-shaped layouts one of the two holds for
+// nearly every group of width <= 5, and the radius is then a fixed half of
+// knp.  Other groups take the runtime select (uniform branches).
+template <int BM1>
+__device__ __forceinline__ uint32_t radius_of(const uint32_t (&knp)[4], uint32_t gm) {
+  const int g = gm_plane(gm);
+  uint32_t r = knp[BM1 >> 1] >> (16 * (BM1 & 1));
+  if (g != BM1) {
+    asm volatile("" : "+v"(r));  // keeps these branches, not selects on every tile
+    if constexpr (BM1 > 0) {
+      if (g == BM1 - 1) return knp[(BM1 - 1) >> 1] >> (16 * ((BM1 - 1) & 1));
+    }
+    r = radius_bits(knp, g);
+  }
+  return r;
+}
+
 // QK of one tile over every present width.
 template <int NSET, int KWB, int... BM1>
 __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const uint8_t* smem,
@@ -548,10 +579,10 @@ __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const
                                        const uint32_t (&gmb)[8], const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
   // (the hi-only variant exists for widths 1 and 2; the flag is uniform)
   ((gmb[BM1] >> 31 ? (BM1 < 2 && ((gmb[BM1] >> 23) & 1u)
-                          ? qk_group<BM1 + 1, NSET, KWB, BM1 < 2>(smem, rw, gmb[BM1],
-                                                                  radius_bits(knp, gm_plane(gmb[BM1])), rep, lane, L)
-                          : qk_group<BM1 + 1, NSET, KWB, false>(smem, rw, gmb[BM1],
-                                                                radius_bits(knp, gm_plane(gmb[BM1])), rep, lane, L))
+                          ? qk_group<BM1 + 1, NSET, KWB, BM1 < 2>(smem, rw, gmb[BM1], radius_of<BM1>(knp, gmb[BM1]),
+                                                                  rep, lane, L)
+                          : qk_group<BM1 + 1, NSET, KWB, false>(smem, rw, gmb[BM1], radius_of<BM1>(knp, gmb[BM1]),
+                                                                rep, lane, L))
                    : void()),
    ...);
 }
@@ -1054,24 +1085,29 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
 #pragma unroll
     for (int s = 0; s < NSET; ++s) {
       float4_t x = L[s];
-      if (!full && (tk >= t_end || tk < t_lo)) x = float4_t{kNegInf, kNegInf, kNegInf, kNegInf};
+      if (!full) {
+        if (tk >= t_end || tk < t_lo) x = float4_t{kNegInf, kNegInf, kNegInf, kNegInf};
+        // (kept a branch: full tiles, nearly all of them, skip the selects)
+        asm volatile("" : "+v"(x));
+      }
       quad_transpose(x, lane);
-      float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-      mx = xmax16(mx);
-      const float mn = fmaxf(m_run[s], mx);
-      const float corr = m_run[s] == kNegInf ? 0.f : exp2_hw(m_run[s] - mn);
-      float ps = 0.f;
+      const float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+      // Most tiles raise no running maximum (one wave-wide vote on this
+      // lane's four scores): the cross-lane maximum, the correction (exactly
+      // 1) and the rescale are then skipped, which changes no result.
+      float mn = m_run[s], corr = 1.f;
+      const bool raise = __builtin_amdgcn_ballot_w64(mx > mn) != 0;
+      if (raise) {
+        mn = fmaxf(mn, xmax16(mx));
+        corr = m_run[s] == kNegInf ? 0.f : exp2_hw(m_run[s] - mn);
+      }
       float p[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        p[r] = exp2_hw(x[r] - mn);
-        ps += p[r];
-      }
+      for (int r = 0; r < 4; ++r) p[r] = exp2_hw(x[r] - mn);
+      const float ps = ((p[0] + p[1]) + p[2]) + p[3];
       pp[s] = as_half4(mix_pair(p[0], p[1], vr.x), mix_pair(p[2], p[3], vr.y));
-      l_run[s] = l_run[s] * corr + ps;  // this lane's tokens only; reduced after the loop
-      // the accumulators are rescaled only when some running maximum moved
-      // (otherwise corr is exactly 1); the test is one wave-wide vote
-      if (__builtin_amdgcn_ballot_w64(mn != m_run[s]) != 0) {
+      l_run[s] = fmaf(l_run[s], corr, ps);  // this lane's tokens only; reduced after the loop
+      if (raise) {
         const float c0 = qperm<0x00>(corr), c1 = qperm<0x55>(corr), c2 = qperm<0xAA>(corr), c3 = qperm<0xFF>(corr);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -1080,8 +1116,8 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
           O[s][h][2] *= c2;
           O[s][h][3] *= c3;
         }
+        m_run[s] = mn;
       }
-      m_run[s] = mn;
     }
 
     // ---------------- PV: 16 steps of 4 tokens (lane = dim)
