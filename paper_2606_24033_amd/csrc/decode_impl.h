@@ -1434,10 +1434,12 @@ hipError_t launch_split_bv_impl(const Dims& d, const void* layout, const void* q
   constexpr int t1 = split_waves<1>() * 64, t2 = split_waves<2>() * 64;
   if (d.group <= 4) {
     if (d.k_words <= 8) go(k_split_mfma<1, 8, BV>, t1);
+    else if (d.k_words <= 12) go(k_split_mfma<1, 12, BV>, t1);
     else if (d.k_words <= 16) go(k_split_mfma<1, 16, BV>, t1);
     else go(k_split_mfma<1, 32, BV>, t1);
   } else {
     if (d.k_words <= 8) go(k_split_mfma<2, 8, BV>, t2);
+    else if (d.k_words <= 12) go(k_split_mfma<2, 12, BV>, t2);
     else if (d.k_words <= 16) go(k_split_mfma<2, 16, BV>, t2);
     else go(k_split_mfma<2, 32, BV>, t2);
   }
