@@ -252,7 +252,7 @@ struct LaneRep {
   uint32_t r4;   // kLut4 + (lane & 7) * 4
   uint32_t r5;   // kLut5 + (lane & 31) * 4
   uint32_t r2;   // kLut2 + (lane & 31) * 8
-  uint32_t r1b;  // kLut1B + (lane & 7) * 16
+  uint32_t r1b;  // kLut1B + (lane & 7) * 16, or kLut1B (the 12-bit table, kernels of 3-bit values)
   uint32_t qimg; // kQimg + lane * 8: this lane's entry in slot 0 of the query image
 };
 
@@ -265,7 +265,7 @@ __device__ __forceinline__ uint32_t lut2_addr(uint32_t w, uint32_t r2) {
 
 // Four consecutive B-bit codes starting at bit POS of w -> four fp16
 // centroids (an MFMA operand).
-template <int B, int POS, int N>
+template <int B, int POS, bool T12, int N>
 __device__ __forceinline__ half4_t decode4(const uint8_t* smem, const uint32_t (&w)[N], const LaneRep& r) {
   if constexpr (B == 2 && POS % 8 == 0) {
     const uint2 u = lds64(smem, lut2_addr<(POS % 32) / 8>(w[POS / 32], r.r2));
@@ -275,6 +275,10 @@ __device__ __forceinline__ half4_t decode4(const uint8_t* smem, const uint32_t (
     return as_half4(u.x, u.y);
   } else if constexpr (B == 1) {
     const uint2 u = lds64(smem, field_at<POS, 4, 7>(w) | r.r1);
+    return as_half4(u.x, u.y);
+  } else if constexpr (B == 3 && T12) {
+    // the 12-bit table: four codes, one lookup (r.r1b holds its base)
+    const uint2 u = lds64(smem, field_at<POS, 12, 3>(w) | r.r1b);
     return as_half4(u.x, u.y);
   } else if constexpr (B == 3) {
     return as_half4(lds32(smem, field_at<POS, 6, 7>(w) | r.r3), lds32(smem, field_at<POS + 6, 6, 7>(w) | r.r3));
@@ -319,12 +323,12 @@ __device__ __forceinline__ void qk_mac(const half4_t& kv, const half4_t (&qh)[NS
 // the row or its zero padding: a valid table index, whose MFMA is skipped),
 // so the decoded operands need no merge copies; wider codes take four
 // lookups a step and are decoded only when the step exists.
-template <int B, int NSET, int K0, int W, int N, bool Z, bool HI>
+template <int B, int NSET, bool T12, int K0, int W, int N, bool Z, bool HI>
 __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&aw)[N], int mm, const LaneRep& rep,
                                           const half4_t (&qh)[NSET], const half4_t (&ql)[NSET],
                                           float4_t (&acc)[NSET]) {
   constexpr int k = 4 * W;
-  if constexpr (B == 1) {
+  if constexpr (B == 1 && !T12) {
     // one 16-byte lookup per code byte: the operands of two steps.  HI: the
     // hi query part only (see qk_group)
     constexpr int by = k / 2;  // byte of step k
@@ -342,10 +346,10 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
       }
     }
   } else if constexpr (B <= 4) {
-    half4_t kv0 = decode4<B, 4 * B * (k + 0)>(smem, aw, rep);
-    half4_t kv1 = decode4<B, 4 * B * (k + 1)>(smem, aw, rep);
-    half4_t kv2 = decode4<B, 4 * B * (k + 2)>(smem, aw, rep);
-    half4_t kv3 = decode4<B, 4 * B * (k + 3)>(smem, aw, rep);
+    half4_t kv0 = decode4<B, 4 * B * (k + 0), T12>(smem, aw, rep);
+    half4_t kv1 = decode4<B, 4 * B * (k + 1), T12>(smem, aw, rep);
+    half4_t kv2 = decode4<B, 4 * B * (k + 2), T12>(smem, aw, rep);
+    half4_t kv3 = decode4<B, 4 * B * (k + 3), T12>(smem, aw, rep);
     // keep the four lookups ahead of the guarded products (one LDS round
     // trip per window): without this the compiler sinks each lookup into
     // the branch that uses it and serialises them
@@ -360,12 +364,12 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
       }
     }
   } else {
-    qk_mac<NSET, K0 + k, true, Z>(decode4<B, 4 * B * k>(smem, aw, rep), qh, ql, acc);
+    qk_mac<NSET, K0 + k, true, Z>(decode4<B, 4 * B * k, T12>(smem, aw, rep), qh, ql, acc);
     if (mm > k + 1) {
-      qk_mac<NSET, K0 + k + 1>(decode4<B, 4 * B * (k + 1)>(smem, aw, rep), qh, ql, acc);
+      qk_mac<NSET, K0 + k + 1>(decode4<B, 4 * B * (k + 1), T12>(smem, aw, rep), qh, ql, acc);
       if (mm > k + 2) {
-        qk_mac<NSET, K0 + k + 2>(decode4<B, 4 * B * (k + 2)>(smem, aw, rep), qh, ql, acc);
-        if (mm > k + 3) qk_mac<NSET, K0 + k + 3>(decode4<B, 4 * B * (k + 3)>(smem, aw, rep), qh, ql, acc);
+        qk_mac<NSET, K0 + k + 2>(decode4<B, 4 * B * (k + 2), T12>(smem, aw, rep), qh, ql, acc);
+        if (mm > k + 3) qk_mac<NSET, K0 + k + 3>(decode4<B, 4 * B * (k + 3), T12>(smem, aw, rep), qh, ql, acc);
       }
     }
   }
@@ -373,7 +377,7 @@ __device__ __forceinline__ void qk_window(const uint8_t* smem, const uint32_t (&
 
 // Sub-chunk SC of a 16-step slot: realign its bits (stream bit ob onwards)
 // to bit 0 of aw, then run its min(CH, ms - SC CH) steps.
-template <int B, int NSET, int KWB, bool Z, bool HI, int SC>
+template <int B, int NSET, bool T12, int KWB, bool Z, bool HI, int SC>
 __device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t (&rw)[KWB + kRowPad], int ob, int ms,
                                              const LaneRep& rep, const half4_t (&qh)[NSET],
                                              const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
@@ -387,18 +391,18 @@ __device__ __forceinline__ void qk_slot_part(const uint8_t* smem, const uint32_t
     for (int i = 0; i < NW; ++i) aw[i] = __builtin_amdgcn_alignbit(rw[w0 + i + 1], rw[w0 + i], sh);
     aw[NW] = 0;
     const int mm = min(CH, ms - SC * CH);
-    qk_window<B, NSET, SC * CH, 0, NW + 1, Z && SC == 0, HI>(smem, aw, mm, rep, qh, ql, acc);
+    qk_window<B, NSET, T12, SC * CH, 0, NW + 1, Z && SC == 0, HI>(smem, aw, mm, rep, qh, ql, acc);
     if constexpr (CH == 8) {
-      if (mm > 4) qk_window<B, NSET, SC * CH, 1, NW + 1, false, HI>(smem, aw, mm, rep, qh, ql, acc);
+      if (mm > 4) qk_window<B, NSET, T12, SC * CH, 1, NW + 1, false, HI>(smem, aw, mm, rep, qh, ql, acc);
     }
   }
 }
 
-template <int B, int NSET, int KWB, bool Z, bool HI, int... SC>
+template <int B, int NSET, bool T12, int KWB, bool Z, bool HI, int... SC>
 __device__ __forceinline__ void qk_slot(std::integer_sequence<int, SC...>, const uint8_t* smem,
                                         const uint32_t (&rw)[KWB + kRowPad], int ob, int ms, const LaneRep& rep,
                                         const half4_t (&qh)[NSET], const half4_t (&ql)[NSET], float4_t (&acc)[NSET]) {
-  (qk_slot_part<B, NSET, KWB, Z, HI, SC>(smem, rw, ob, ms, rep, qh, ql, acc), ...);
+  (qk_slot_part<B, NSET, T12, KWB, Z, HI, SC>(smem, rw, ob, ms, rep, qh, ql, acc), ...);
 }
 
 // The group of width B (metadata gm, radius bits nrm16 of the lane's token):
@@ -409,7 +413,7 @@ __device__ __forceinline__ void qk_slot(std::integer_sequence<int, SC...>, const
 // attention output by <= 3.4e-4 (relative) on the Llama-shaped workload.  A
 // row whose low widths carry most of the energy (a uniform 1- or 2-bit
 // layout) keeps both parts: fp16 queries alone cost ~3e-3 there.
-template <int B, int NSET, int KWB, bool HI>
+template <int B, int NSET, bool T12, int KWB, bool HI>
 __device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&rw)[KWB + kRowPad], uint32_t gm,
                                          uint32_t nrm16, const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
   const int o = gm_off(gm), nst = gm_steps(gm), slot0 = gm_slot(gm);
@@ -424,7 +428,7 @@ __device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&r
       qh[s] = as_half4(uh.x, uh.y);
       ql[s] = as_half4(ul.x, ul.y);
     }
-    qk_slot<B, NSET, KWB, decltype(first)::value, HI>(std::make_integer_sequence<int, 16 / qk_ch<B>()>{}, smem, rw,
+    qk_slot<B, NSET, T12, KWB, decltype(first)::value, HI>(std::make_integer_sequence<int, 16 / qk_ch<B>()>{}, smem, rw,
                                                       o + 64 * B * c, min(16, nst - 16 * c), rep, qh, ql, acc);
   };
   slot(std::true_type{}, 0);
@@ -440,23 +444,23 @@ __device__ __forceinline__ void qk_group(const uint8_t* smem, const uint32_t (&r
 template <int BV>
 constexpr int pv_words() { return BV; }
 
-template <int BV, int NSET, int S>
+template <int BV, int NSET, bool T12, int S>
 __device__ __forceinline__ void pv_step(const uint8_t* smem, const uint32_t (&vw)[4][pv_words<BV>()],
                                         const LaneRep& rep, const half4_t (&pp)[NSET], float4_t (&O)[NSET][2]) {
   constexpr int tau = S >> 3, sp = S & 7;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const half4_t vv = decode4<BV, 4 * BV * sp>(smem, vw[tau * 2 + h], rep);
+    const half4_t vv = decode4<BV, 4 * BV * sp, T12>(smem, vw[tau * 2 + h], rep);
 #pragma unroll
     for (int s = 0; s < NSET; ++s) O[s][h] = __builtin_amdgcn_mfma_f32_4x4x4f16(pp[s], vv, O[s][h], 4, S, 0);
   }
 }
 
-template <int BV, int NSET, int... S>
+template <int BV, int NSET, bool T12, int... S>
 __device__ __forceinline__ void pv_steps(std::integer_sequence<int, S...>, const uint8_t* smem,
                                          const uint32_t (&vw)[4][pv_words<BV>()], const LaneRep& rep,
                                          const half4_t (&pp)[NSET], float4_t (&O)[NSET][2]) {
-  (pv_step<BV, NSET, S>(smem, vw, rep, pp, O), ...);
+  (pv_step<BV, NSET, T12, S>(smem, vw, rep, pp, O), ...);
 }
 
 // ---------------------------------------------------------------- loads
@@ -573,15 +577,15 @@ __device__ __forceinline__ uint32_t radius_of(const uint32_t (&knp)[4], uint32_t
 }
 
 // QK of one tile over every present width.
-template <int NSET, int KWB, int... BM1>
+template <int NSET, bool T12, int KWB, int... BM1>
 __device__ __forceinline__ void qk_all(std::integer_sequence<int, BM1...>, const uint8_t* smem,
                                        const uint32_t (&rw)[KWB + kRowPad], const uint32_t (&knp)[4],
                                        const uint32_t (&gmb)[8], const LaneRep& rep, int lane, float4_t (&L)[NSET]) {
   // (the hi-only variant exists for widths 1 and 2; the flag is uniform)
   ((gmb[BM1] >> 31 ? (BM1 < 2 && ((gmb[BM1] >> 23) & 1u)
-                          ? qk_group<BM1 + 1, NSET, KWB, BM1 < 2>(smem, rw, gmb[BM1], radius_of<BM1>(knp, gmb[BM1]),
+                          ? qk_group<BM1 + 1, NSET, T12, KWB, BM1 < 2>(smem, rw, gmb[BM1], radius_of<BM1>(knp, gmb[BM1]),
                                                                   rep, lane, L)
-                          : qk_group<BM1 + 1, NSET, KWB, false>(smem, rw, gmb[BM1], radius_of<BM1>(knp, gmb[BM1]),
+                          : qk_group<BM1 + 1, NSET, T12, KWB, false>(smem, rw, gmb[BM1], radius_of<BM1>(knp, gmb[BM1]),
                                                                 rep, lane, L))
                    : void()),
    ...);
@@ -765,6 +769,10 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
     int split_len, WinArgs win) {
   // this instantiation's workgroup (shadows the 16-wave default)
   constexpr int kWaves = split_waves<NSET>(), kThreads = kWaves * 64;
+  // kernels of 3-bit values hold the 3-bit codes' 12-bit table (one lookup
+  // per four codes, values and keys) where the others hold the 1-bit keys'
+  // byte table
+  constexpr bool T12 = BV == 3;
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: tile addresses stay scalar
@@ -923,12 +931,23 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
         make_uint2(cb[e & 1] | (static_cast<uint32_t>(cb[(e >> 1) & 1]) << 16),
                    cb[(e >> 2) & 1] | (static_cast<uint32_t>(cb[(e >> 3) & 1]) << 16));
   }
+  if constexpr (T12) {
+    // 3-bit codes four at a time, in the byte table's place: entry i holds
+    // the centroids of codes i & 7, (i >> 3) & 7, (i >> 6) & 7 and i >> 9
+    // (one copy; 1-bit key codes then take the 4-code table)
+    const uint16_t* cb = cbs + cb_index(3);
+    for (int i = tid; i < 4096; i += kThreads)
+      *reinterpret_cast<uint2*>(smem + kLut1B + i * 8) =
+          make_uint2(cb[i & 7] | (static_cast<uint32_t>(cb[(i >> 3) & 7]) << 16),
+                     cb[(i >> 6) & 7] | (static_cast<uint32_t>(cb[i >> 9]) << 16));
+  } else {
 #pragma unroll
-  for (int i = tid; i < 256 * 8; i += kThreads) {
-    const int e = i >> 3;  // code byte: bit c is the code of coordinate c
-    const uint16_t* cb = cbs + cb_index(1);
-    const auto pair = [&](int c) { return cb[(e >> c) & 1] | (static_cast<uint32_t>(cb[(e >> (c + 1)) & 1]) << 16); };
-    *reinterpret_cast<uint4*>(smem + kLut1B + i * 16) = make_uint4(pair(0), pair(2), pair(4), pair(6));
+    for (int i = tid; i < 256 * 8; i += kThreads) {
+      const int e = i >> 3;  // code byte: bit c is the code of coordinate c
+      const uint16_t* cb = cbs + cb_index(1);
+      const auto pair = [&](int c) { return cb[(e >> c) & 1] | (static_cast<uint32_t>(cb[(e >> (c + 1)) & 1]) << 16); };
+      *reinterpret_cast<uint4*>(smem + kLut1B + i * 16) = make_uint4(pair(0), pair(2), pair(4), pair(6));
+    }
   }
 #pragma unroll
   for (int i = tid; i < 256 * 32; i += kThreads) {
@@ -964,7 +983,7 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
   uint32_t gmb[8];
   LaneRep rep{static_cast<uint32_t>(kLut1 + (lane & 15) * 8), static_cast<uint32_t>(kLut3 + (lane & 31) * 4),
                     static_cast<uint32_t>(kLut4 + (lane & 7) * 4),   static_cast<uint32_t>(kLut5 + (lane & 31) * 4),
-                    static_cast<uint32_t>(kLut2 + (lane & 31) * 8),  static_cast<uint32_t>(kLut1B + (lane & 7) * 16),
+                    static_cast<uint32_t>(kLut2 + (lane & 31) * 8),  static_cast<uint32_t>(kLut1B + (T12 ? 0 : (lane & 7) * 16)),
                     static_cast<uint32_t>(kQimg + lane * 8)};
   // opaque to the compiler: with the bits of the bases unknown, a lookup
   // address stays (shifted field & mask) | base, one and-or
@@ -1063,7 +1082,7 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
 #pragma unroll
     for (int s = 0; s < NSET; ++s) L[s] = float4_t{0.f, 0.f, 0.f, 0.f};
     __builtin_amdgcn_s_setprio(2);
-    qk_all<NSET, KWB>(std::make_integer_sequence<int, 8>{}, smem, rw, knp, gmb, rep, lane, L);
+    qk_all<NSET, T12, KWB>(std::make_integer_sequence<int, 8>{}, smem, rw, knp, gmb, rep, lane, L);
     __builtin_amdgcn_s_setprio(0);
 
     // ---------------- online softmax (lane 4b+i: head i, tokens 4b..4b+3)
@@ -1122,7 +1141,7 @@ __attribute__((amdgpu_waves_per_eu(NSET == 1 && KWB <= 16 ? 4 : 3))) void k_spli
 
     // ---------------- PV: 16 steps of 4 tokens (lane = dim)
     __builtin_amdgcn_s_setprio(1);
-    pv_steps<BV, NSET>(std::make_integer_sequence<int, 16>{}, smem, vw, rep, pp, O);
+    pv_steps<BV, NSET, T12>(std::make_integer_sequence<int, 16>{}, smem, vw, rep, pp, O);
     __builtin_amdgcn_s_setprio(0);
   }
 

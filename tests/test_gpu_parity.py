@@ -570,11 +570,14 @@ def test_argument_errors_on_device():
 
 
 @pytest.mark.parametrize("G,v_bits,k_budget", [(1, 5, 192), (2, 6, 256), (3, 7, 128), (5, 5, 192), (6, 6, 160),
-                                                (7, 7, 224), (3, 1, 64), (6, 4, 320)])
+                                                (7, 7, 224), (3, 1, 64), (6, 4, 320), (4, 3, 128), (8, 3, 128),
+                                                (2, 3, 160)])
 def test_decode_query_groups_and_value_widths(G, v_bits, k_budget):
     """Decode attention (Sec. 4) for GQA groups of 1-7 query heads (a partial
     first set of four heads for G < 4; a partial second set for G = 5..7) and
-    value widths 1 and 4-7, over key rows of 8, 10, 12, 16 and 20 words:
+    value widths 1 and 3-7, over key rows of 8, 10, 12, 16 and 20 words (the
+    3-bit cases hold 1-bit key groups, which kernels of 3-bit values decode
+    with the 4-code table instead of the byte table):
     2 layers x batch 2 x 2 KV heads, bf16, contexts 1300 and 77 rows,
     all-layer calls with 0, 1 and 3 splits and single-layer calls that must
     give the same bits at 1 and 3 splits.  Codes and radii
