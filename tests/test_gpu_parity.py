@@ -690,16 +690,18 @@ def test_llama_128k_step_whole_layer(llama_128k, layer):
     assert stats.code_ties <= 1e-4 * stats.codes
 
 
-def test_protected_window_decode():
+@pytest.mark.parametrize("k_budget,v_bits,G", [(128, 2, 4), (192, 3, 8)])
+def test_protected_window_decode(k_budget, v_bits, G):
     """Protected-buffer regime (sink 4 + recent 128 fp16 rows beside the packed
     cache, and the 63 + 1 and 0 + 0 edges): a 100-row prefill that the window
     covers (no packed rows), a 300-row chunk that overruns the recent ring, then
     single-row decode appends; all-layer and single-layer calls, one and three
     splits; against the oracle's protected attention within 2e-3, and the empty
-    window bit-identical to the plain packed decode."""
+    window bit-identical to the plain packed decode.  K2V2 with one query set of
+    4 heads, and K3V3 with two sets of 8 (the 3-bit values' 12-bit table)."""
     bg = bgm()
-    st = P.make_setup(11, 2, 2, 2, 4, 1024, 128, 2, 5e5, "bf16")
-    L, B, H, G = st.cfg.n_layers, st.cfg.batch, st.cfg.n_kv_heads, st.cfg.group
+    st = P.make_setup(11, 2, 2, 2, G, 1024, k_budget, v_bits, 5e5, "bf16")
+    L, B, H = st.cfg.n_layers, st.cfg.batch, st.cfg.n_kv_heads
     layout, cache = build(st)
     windows = {(ns, nr): torch.zeros(bg.window_bytes(st.cfg, ns, nr) // 2, dtype=torch.float16, device="cuda")
                for ns, nr in [(4, 128), (63, 1), (0, 0)]}
