@@ -19,14 +19,17 @@ def _dev(x):
     return t.to(device="cuda", dtype=torch.bfloat16).contiguous()
 
 
-def test_noalloc_decode_matches_workspace_entry_point():
+@pytest.mark.parametrize("G,v_bits", [(4, 2), (8, 3)])
+def test_noalloc_decode_matches_workspace_entry_point(G, v_bits):
+    """K3V2 with one query set of 4 heads, and K3V3 with two sets of 8 (the
+    12-bit table of 3-bit codes)."""
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_2606_24033_amd import blockgtq as bg
     bg.lib()
-    L, B, H, G = 2, 2, 2, 4
+    L, B, H = 2, 2, 2
     lens = [1400, 300]
-    st = P.make_setup(61, L, B, H, G, 1408, 192, 2, 5e5, "bf16")
+    st = P.make_setup(61, L, B, H, G, 1408, 192, v_bits, 5e5, "bf16")
     assert np.array_equal(st.bits, st.bits_oracle)
     layout = bg.Layout(st.cfg, st.bits, synth.flat_rot_k(st.rot_k), st.rot_v)
     cache = bg.Cache(st.cfg)
